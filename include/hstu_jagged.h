@@ -1,0 +1,167 @@
+/*
+ * hstu_jagged.h -- C ABI of the MI355X (gfx950) jagged HSTU attention library.
+ *
+ * Operation.  The paper's jagged fusion operator for attention and RAB
+ * (Sec. 3.1.1 "Jagged Fusion Operators for Attention and RAB" and the
+ * appendix of the same name) fuses attention with a relative attention bias
+ * -- relative position bias (rpb) plus relative time bias (rtb) -- over
+ * jagged query/key/value inputs, with no padding and no dense<->jagged
+ * conversion at the operator boundary.  For HSTU-style models (Appendix A,
+ * "Parameter Settings": bucketized time encodings and relative positional
+ * encodings) this library computes, for every sequence b with rows
+ * off[b] .. off[b+1]-1, every head h and local positions i, j:
+ *
+ *   s_ij = <q_i, k_j> + pos_w[h, j - i + N - 1] + time_w[h, bucket(ts_i - ts_j)]
+ *   a_ij = silu(s_ij) / N   for j <= i (causal), else 0;   N = max_len
+ *   o_i  = sum_j a_ij v_j                                    (per head)
+ *   y    = LayerNorm(o) * u   per token over all H*d features
+ *          (biased variance, eps = HSTU_LN_EPS, no affine parameters)
+ *
+ * bucket(x): |x| < 4 -> |x|; else with e = floor(log2 |x|),
+ * 4*(e-1) + ((|x| >> (e-2)) & 3), clamped to num_buckets-1 (four log-spaced
+ * buckets per octave; the paper names bucketized time encodings without
+ * giving the rule, this is the library's reading).
+ *
+ * The backward pass returns dq, dk, dv, du and the table gradients d_pos_w,
+ * d_time_w of sum(y * dy).
+ *
+ * Layout.  Every tensor is row-major and contiguous.  q, k, v, u, o, dq, dk,
+ * dv, du and dO are [T][H][d]; y and dy are [T][H*d] (the same memory
+ * layout: head h occupies columns h*d .. h*d+d-1 of a row).  T is the total
+ * number of tokens, seq_offsets[B].
+ *
+ * Pointers.  Every tensor pointer is a DEVICE pointer on the current HIP
+ * device; the caller owns all memory.  The library never allocates device
+ * memory and never synchronises: each call enqueues its kernels on `stream`
+ * (a hipStream_t; NULL = the default stream) and returns.  Buffers must stay
+ * alive until that work completes.
+ *
+ * seq_offsets contract (int64, device): off[0] = 0, non-decreasing,
+ * 0 <= off[b+1] - off[b] <= max_len, off[B] = total_tokens.  It is read on
+ * the device only and is not checked; the kernels clamp each length into
+ * [0, max_len] and each row index into [0, total_tokens), so a violating
+ * offsets array yields unspecified values but never an out-of-bounds access.
+ * Empty sequences are legal.  B = 0 or total_tokens = 0 is a successful
+ * call; it enqueues nothing, except that a backward call with a bias table
+ * still writes that table's gradient (all zeros).
+ *
+ * Precision.  HSTU_BF16: q, k, v, u, dy and all tensor outputs are bfloat16,
+ * tables and LayerNorm statistics are float32; contractions run on bf16 MFMA
+ * with float32 accumulation, a_ij and dS_ij are rounded to bf16 only as MFMA
+ * operands; d in {64, 128}.  HSTU_F32: every tensor is float32 and all
+ * arithmetic is float32; d in {32, 64, 128}.
+ *
+ * Return codes: 0 on success, else one of the negative HSTU_E* codes below;
+ * hstu_last_error() then describes the failure (thread-local string owned by
+ * the library, valid until the next call on the same thread).
+ */
+#ifndef HSTU_JAGGED_H
+#define HSTU_JAGGED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HSTU_OK 0
+#define HSTU_EINVAL (-1)      /* null required pointer, bad size or dtype    */
+#define HSTU_ENOTSUP (-2)     /* valid but unsupported (e.g. bf16 with d=32) */
+#define HSTU_EWORKSPACE (-3)  /* workspace missing or too small              */
+#define HSTU_EHIP (-4)        /* a HIP runtime call or a launch failed        */
+
+#define HSTU_LN_EPS 1e-6f
+
+typedef enum { HSTU_BF16 = 0, HSTU_F32 = 1 } hstu_dtype;
+
+/* Relative attention bias (Sec. 3.1.1: rpb + rtb).  Either table may be
+ * NULL; with both NULL the bias is zero. */
+typedef struct {
+    const float *pos_w;          /* [H][2*max_len-1] float32, or NULL        */
+    const float *time_w;         /* [H][num_buckets] float32, or NULL        */
+    const int64_t *timestamps;   /* [T] int64; required iff time_w != NULL   */
+    int32_t num_buckets;         /* >= 1 iff time_w != NULL; H*num_buckets
+                                    <= 4096 for HSTU_BF16                     */
+} hstu_rab;
+
+/* Forward outputs and scratch, all caller-allocated.  o, ln_mean and
+ * ln_rstd are the saved state the backward pass consumes. */
+typedef struct {
+    hstu_dtype dtype;            /* element type of q, k, v, u, y, o         */
+    int64_t total_tokens;        /* T = seq_offsets[B]                       */
+    void *y;                     /* [T][H*d]   LayerNorm(o) * u              */
+    void *o;                     /* [T][H][d]  attention output (pre-norm)   */
+    float *ln_mean;              /* [T]                                      */
+    float *ln_rstd;              /* [T]  1/sqrt(var + eps)                   */
+    void *workspace;             /* device scratch, 256-byte aligned         */
+    size_t workspace_bytes;      /* >= hstu_jagged_attn_workspace_bytes(..,0) */
+} hstu_fwd_out;
+
+/* Backward inputs (saved forward state + upstream gradient), gradient
+ * outputs and scratch.  Gradients are overwritten, never accumulated; table
+ * entries no causal pair reaches are written as 0. */
+typedef struct {
+    hstu_dtype dtype;
+    int64_t total_tokens;        /* T = seq_offsets[B]                       */
+    const void *dy;              /* [T][H*d]                                 */
+    const void *o;               /* [T][H][d]  from the forward              */
+    const float *ln_mean;        /* [T]        from the forward              */
+    const float *ln_rstd;        /* [T]        from the forward              */
+    void *dq, *dk, *dv;          /* [T][H][d]                                */
+    void *du;                    /* [T][H*d]                                 */
+    float *d_pos_w;              /* [H][2*max_len-1]; required iff pos_w     */
+    float *d_time_w;             /* [H][num_buckets]; required iff time_w    */
+    void *workspace;             /* device scratch, 256-byte aligned         */
+    size_t workspace_bytes;      /* >= hstu_jagged_attn_workspace_bytes(..,1) */
+} hstu_bwd_io;
+
+/* Forward: o, y, ln_mean, ln_rstd from q, k, v, u (Sec. 3.1.1). */
+int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
+                         const void *u, const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int32_t H, int32_t d,
+                         const hstu_rab *rab, hstu_fwd_out *out, void *stream);
+
+/* Backward: dq, dk, dv, du, d_pos_w, d_time_w of sum(y * dy), given the
+ * forward's saved o / ln_mean / ln_rstd (Sec. 3.1.1; the table gradients are
+ * the paper's "RAB backward"). */
+int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
+                         const void *u, const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int32_t H, int32_t d,
+                         const hstu_rab *rab, hstu_bwd_io *io, void *stream);
+
+/* Bytes of device workspace a forward (for_bwd = 0) or backward
+ * (for_bwd = 1) call needs for these sizes; depends on the current device's
+ * compute-unit count.  Returns 0 for invalid sizes (see hstu_last_error). */
+size_t hstu_jagged_attn_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
+                                        int32_t d, int64_t total_tokens,
+                                        int32_t for_bwd, hstu_dtype dtype,
+                                        const hstu_rab *rab);
+
+/* Runs only the seq_offsets tile scheduler (the first step of both calls)
+ * and copies its work lists out, for inspection and tests.  Work is split
+ * into (sequence, 64-row tile) entries; the q-list orders query tiles by
+ * their causal cost (tile index + 1 key tiles), the k-list orders key tiles
+ * by theirs (tiles of the sequence minus tile index), both longest first --
+ * the sort-by-cost, assign-greedily balancing of Sec. 3.1.3 applied to the
+ * compute units of one GPU.  Device pointers: n_entries [1] int32 receives
+ * the entry count E; list_q and list_k receive E int32 pairs
+ * (sequence, tile) in pop order and must hold
+ * min(B*ceil(max_len/64), (total_tokens + 63*B)/64) pairs.  workspace_bytes
+ * must be >= hstu_jagged_attn_workspace_bytes(B, max_len, 1, 64,
+ * total_tokens, 1, HSTU_F32, NULL).  Asynchronous on `stream`. */
+int hstu_jagged_schedule(const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int64_t total_tokens,
+                         int32_t *n_entries, int32_t *list_q, int32_t *list_k,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Thread-local description of the last failure ("" if none). */
+const char *hstu_last_error(void);
+
+/* Library version string. */
+const char *hstu_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HSTU_JAGGED_H */

@@ -1,0 +1,289 @@
+// C ABI of the jagged HSTU attention library: argument validation, workspace
+// carving and the launch sequence of each call.  No call allocates device
+// memory or synchronises; every kernel goes onto the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace hstu {
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+  return fail(HSTU_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Validates everything the host can see; on success fills `p`.
+int validate(const void *q, const void *k, const void *v, const void *u,
+             const int64_t *off, int32_t B, int32_t N, int32_t H, int32_t d,
+             const hstu_rab *rab, hstu_dtype dtype, int64_t T, Problem *p) {
+  if (dtype != HSTU_BF16 && dtype != HSTU_F32)
+    return fail(HSTU_EINVAL, "dtype %d is not HSTU_BF16 or HSTU_F32", (int)dtype);
+  if (B < 0) return fail(HSTU_EINVAL, "B = %d < 0", B);
+  if (T < 0) return fail(HSTU_EINVAL, "total_tokens = %lld < 0", (long long)T);
+  if (B == 0 && T != 0)
+    return fail(HSTU_EINVAL, "B = 0 but total_tokens = %lld", (long long)T);
+  if (N < 1) return fail(HSTU_EINVAL, "max_len = %d < 1", N);
+  if (H < 1) return fail(HSTU_EINVAL, "H = %d < 1", H);
+  if (d != 32 && d != 64 && d != 128)
+    return fail(HSTU_EINVAL, "d = %d is not 32, 64 or 128", d);
+  if (dtype == HSTU_BF16 && d == 32)
+    return fail(HSTU_ENOTSUP, "bf16 path supports d = 64 or 128, got 32");
+  if (N > 65536) return fail(HSTU_ENOTSUP, "max_len = %d > 65536", N);
+  if (H > 64) return fail(HSTU_ENOTSUP, "H = %d > 64", H);
+  if (!off) return fail(HSTU_EINVAL, "seq_offsets must be non-null");
+  if (T > 0 && (!q || !k || !v || !u))
+    return fail(HSTU_EINVAL, "q, k, v, u must be non-null when total_tokens > 0");
+  const bool has_pos = rab && rab->pos_w;
+  const bool has_time = rab && rab->time_w;
+  int32_t nb = 0;
+  if (has_time) {
+    if (!rab->timestamps)
+      return fail(HSTU_EINVAL, "rab->time_w given without rab->timestamps");
+    if (rab->num_buckets < 1)
+      return fail(HSTU_EINVAL, "rab->num_buckets = %d < 1", rab->num_buckets);
+    nb = rab->num_buckets;
+    if (dtype == HSTU_BF16 && (int64_t)H * nb > 4096)
+      return fail(HSTU_ENOTSUP, "H * num_buckets = %lld > 4096",
+                  (long long)H * nb);
+  }
+  p->B = B; p->N = N; p->H = H; p->d = d; p->T = T; p->dtype = dtype;
+  p->has_pos = has_pos; p->has_time = has_time; p->nb = nb;
+  // sum_b ceil(L_b/64) <= min(B * ceil(N/64), floor((T + 63 B) / 64))
+  p->max_entries = std::min<int64_t>((int64_t)B * ceil_div(N, TILE),
+                                     (T + (int64_t)(TILE - 1) * B) / TILE);
+  return HSTU_OK;
+}
+
+int check_workspace(const Layout &L, void *ws, size_t bytes) {
+  if (!ws) return fail(HSTU_EWORKSPACE, "workspace is NULL (%zu bytes needed)", L.total);
+  if ((uintptr_t)ws % kAlign)
+    return fail(HSTU_EINVAL, "workspace is not %zu-byte aligned", kAlign);
+  if (bytes < L.total)
+    return fail(HSTU_EWORKSPACE, "workspace has %zu bytes, %zu needed", bytes, L.total);
+  return HSTU_OK;
+}
+
+int current_device(int *dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  return HSTU_OK;
+}
+
+}  // namespace
+
+const DeviceInfo &device_info(int dev) {
+  static std::mutex mu;
+  static std::vector<DeviceInfo> cache;
+  static std::vector<bool> have;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)cache.size() <= dev) {
+    cache.resize(dev + 1);
+    have.resize(dev + 1, false);
+  }
+  if (!have[dev]) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cu <= 0)
+      cu = 256;
+    cache[dev].num_cu = cu;
+    have[dev] = true;
+  }
+  return cache[dev];
+}
+
+Layout make_layout(const Problem &p, bool for_bwd, int dev) {
+  Layout L{};
+  size_t at = 0;
+  auto take = [&](size_t bytes) {
+    size_t off = at;
+    at += align_up(bytes);
+    return off;
+  };
+  const size_t elem = p.dtype == HSTU_BF16 ? 2 : 4;
+  L.ctrl = take(sizeof(int32_t) * CTRL_WORDS);
+  L.seqinfo = take(sizeof(SeqInfo) * (size_t)std::max(p.B, 1));
+  L.list_q = take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1));
+  L.list_k = for_bwd ? take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
+  L.dO = for_bwd ? take(elem * (size_t)p.T * p.H * p.d) : 0;
+  const bool bf16_bwd = for_bwd && p.dtype == HSTU_BF16;
+  L.dkv_grid = bf16_bwd ? attn_dkv_grid(p, dev) : 0;
+  L.dpos_part = (bf16_bwd && p.has_pos) ? take(sizeof(float) * (size_t)p.T * p.H) : 0;
+  L.dtime_part = (bf16_bwd && p.has_time)
+                     ? take(sizeof(float) * (size_t)L.dkv_grid * p.H * p.nb)
+                     : 0;
+  L.total = at;
+  return L;
+}
+
+}  // namespace hstu
+
+using namespace hstu;
+
+extern "C" {
+
+const char *hstu_last_error(void) { return g_last_error.c_str(); }
+
+const char *hstu_version(void) { return "hstu_jagged 0.1 gfx950"; }
+
+size_t hstu_jagged_attn_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
+                                        int32_t d, int64_t total_tokens,
+                                        int32_t for_bwd, hstu_dtype dtype,
+                                        const hstu_rab *rab) {
+  Problem p;
+  static const char dummy = 0;
+  g_last_error.clear();
+  if (validate(&dummy, &dummy, &dummy, &dummy, (const int64_t *)&dummy, B,
+               max_len, H, d, rab, dtype, total_tokens, &p) != HSTU_OK)
+    return 0;
+  int dev = 0;
+  if (current_device(&dev) != HSTU_OK) return 0;
+  return make_layout(p, for_bwd != 0, dev).total;
+}
+
+int hstu_jagged_schedule(const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int64_t total_tokens,
+                         int32_t *n_entries, int32_t *list_q, int32_t *list_k,
+                         void *workspace, size_t workspace_bytes, void *stream) {
+  g_last_error.clear();
+  Problem p;
+  static const char dummy = 0;
+  int rc = validate(&dummy, &dummy, &dummy, &dummy, seq_offsets, B, max_len, 1,
+                    64, nullptr, HSTU_F32, total_tokens, &p);
+  if (rc != HSTU_OK) return rc;
+  if (!n_entries || (p.max_entries > 0 && (!list_q || !list_k)))
+    return fail(HSTU_EINVAL, "n_entries, list_q and list_k must be non-null");
+  int dev = 0;
+  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
+  Layout L = make_layout(p, true, dev);
+  if ((rc = check_workspace(L, workspace, workspace_bytes)) != HSTU_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = launch_schedule(seq_offsets, p, workspace, L, s);
+  if (e != hipSuccess) return hip_fail(e, "schedule launch");
+  const char *ws = (const char *)workspace;
+  const size_t list_bytes = sizeof(WorkEntry) * (size_t)p.max_entries;
+  e = hipMemcpyAsync(n_entries, ws + L.ctrl + sizeof(int32_t) * CTRL_N_ENTRIES,
+                     sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && list_bytes)
+    e = hipMemcpyAsync(list_q, ws + L.list_q, list_bytes, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && list_bytes)
+    e = hipMemcpyAsync(list_k, ws + L.list_k, list_bytes, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "work-list copy");
+  return HSTU_OK;
+}
+
+int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
+                         const void *u, const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int32_t H, int32_t d,
+                         const hstu_rab *rab, hstu_fwd_out *out, void *stream) {
+  g_last_error.clear();
+  if (!out) return fail(HSTU_EINVAL, "out is NULL");
+  Problem p;
+  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, out->dtype,
+                    out->total_tokens, &p);
+  if (rc != HSTU_OK) return rc;
+  if (p.T > 0 && (!out->y || !out->o || !out->ln_mean || !out->ln_rstd))
+    return fail(HSTU_EINVAL, "out->y, o, ln_mean and ln_rstd must be non-null");
+  if (p.T == 0) return HSTU_OK;
+  int dev = 0;
+  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
+  Layout L = make_layout(p, false, dev);
+  if ((rc = check_workspace(L, out->workspace, out->workspace_bytes)) != HSTU_OK)
+    return rc;
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a{q, k, v, u,
+             rab ? rab->pos_w : nullptr,
+             p.has_time ? rab->time_w : nullptr,
+             p.has_time ? rab->timestamps : nullptr,
+             out->workspace, L, p};
+  hipError_t e = launch_schedule(seq_offsets, p, out->workspace, L, s);
+  if (e != hipSuccess) return hip_fail(e, "schedule launch");
+  e = p.dtype == HSTU_BF16 ? launch_attn_fwd_bf16(a, out->o, s)
+                           : launch_attn_fwd_f32(a, out->o, s);
+  if (e != hipSuccess) return hip_fail(e, "attention forward launch");
+  e = launch_ln_fwd(p, out->o, u, out->y, out->ln_mean, out->ln_rstd, s);
+  if (e != hipSuccess) return hip_fail(e, "layernorm forward launch");
+  return HSTU_OK;
+}
+
+int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
+                         const void *u, const int64_t *seq_offsets, int32_t B,
+                         int32_t max_len, int32_t H, int32_t d,
+                         const hstu_rab *rab, hstu_bwd_io *io, void *stream) {
+  g_last_error.clear();
+  if (!io) return fail(HSTU_EINVAL, "io is NULL");
+  Problem p;
+  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, io->dtype,
+                    io->total_tokens, &p);
+  if (rc != HSTU_OK) return rc;
+  if (p.T > 0 && (!io->dy || !io->o || !io->ln_mean || !io->ln_rstd || !io->dq ||
+                  !io->dk || !io->dv || !io->du))
+    return fail(HSTU_EINVAL, "io->dy, o, ln_mean, ln_rstd, dq, dk, dv, du must be non-null");
+  if (p.has_pos && !io->d_pos_w)
+    return fail(HSTU_EINVAL, "rab->pos_w given but io->d_pos_w is NULL");
+  if (p.has_time && !io->d_time_w)
+    return fail(HSTU_EINVAL, "rab->time_w given but io->d_time_w is NULL");
+  if (p.T == 0 && !p.has_pos && !p.has_time) return HSTU_OK;
+  int dev = 0;
+  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
+  Layout L = make_layout(p, true, dev);
+  if ((rc = check_workspace(L, io->workspace, io->workspace_bytes)) != HSTU_OK)
+    return rc;
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a{q, k, v, u,
+             rab ? rab->pos_w : nullptr,
+             p.has_time ? rab->time_w : nullptr,
+             p.has_time ? rab->timestamps : nullptr,
+             io->workspace, L, p};
+  char *ws = (char *)io->workspace;
+  float *d_pos = p.has_pos ? io->d_pos_w : nullptr;
+  float *d_time = p.has_time ? io->d_time_w : nullptr;
+  hipError_t e = launch_schedule(seq_offsets, p, ws, L, s);
+  if (e != hipSuccess) return hip_fail(e, "schedule launch");
+  if (p.T > 0) {
+    e = launch_ln_bwd(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
+                      ws + L.dO, L.dpos_part ? (float *)(ws + L.dpos_part) : nullptr, s);
+    if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
+  }
+  if (p.dtype == HSTU_BF16) {
+    if (p.T > 0) {
+      e = launch_attn_dq_bf16(a, ws + L.dO, io->dq, s);
+      if (e != hipSuccess) return hip_fail(e, "attention dQ launch");
+    }
+    e = launch_attn_dkv_bf16(a, ws + L.dO, io->dk, io->dv, s);
+    if (e != hipSuccess) return hip_fail(e, "attention dK/dV launch");
+    e = launch_finalize_tables(a, d_pos, d_time, s);
+    if (e != hipSuccess) return hip_fail(e, "table finalize launch");
+  } else {
+    e = launch_attn_bwd_f32(a, ws + L.dO, io->dq, io->dk, io->dv, d_pos, d_time, s);
+    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
+  }
+  return HSTU_OK;
+}
+
+}  // extern "C"

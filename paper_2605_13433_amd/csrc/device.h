@@ -1,0 +1,76 @@
+// Device-side helpers shared by the gfx950 kernels of the jagged HSTU
+// attention library: MFMA operand types, bf16 packing, the relative-time
+// bucket rule and SiLU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hstu {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16;
+
+// 32x32x16 bf16 MFMA, fp32 accumulate.  Operand layout (wave64):
+//   A [32 x 16]: lane l holds row l%32, k-slots 8*(l/32) .. +7
+//   B [16 x 32]: lane l holds col l%32, k-slots 8*(l/32) .. +7
+//   C [32 x 32]: lane l holds col l%32, rows 8*(r/4) + 4*(l/32) + r%4, r=0..15
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Row index (within a 32x32 C block) of accumulator register r of lane group g.
+__device__ __forceinline__ constexpr int c_row(int r, int g) {
+  return 8 * (r >> 2) + 4 * g + (r & 3);
+}
+
+// bf16 bits -> float.
+__device__ __forceinline__ float bf2f(u16 x) {
+  return __uint_as_float(((uint32_t)x) << 16);
+}
+
+// Two floats -> packed bf16 pair (round to nearest even, hardware cvt).
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 r;
+  r[0] = (__bf16)a;
+  r[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) {
+  return __builtin_bit_cast(bf16x8, x);
+}
+
+__device__ __forceinline__ bf16x8 join8(uint2 lo, uint2 hi) {
+  uint4 x;
+  x.x = lo.x; x.y = lo.y; x.z = hi.x; x.w = hi.y;
+  return __builtin_bit_cast(bf16x8, x);
+}
+
+// Relative-time bucket: |x| < 4 -> |x|; otherwise four log-spaced buckets per
+// octave, 4*(e-1) + (two bits below the leading one) with e = floor(log2|x|);
+// clamped to nb-1.  Integer-only, so every device and the host agree.
+__device__ __forceinline__ int time_bucket(int64_t delta, int nb) {
+  uint64_t x = delta < 0 ? (uint64_t)0 - (uint64_t)delta : (uint64_t)delta;
+  int b;
+  if (x < 4) {
+    b = (int)x;
+  } else {
+    int e = 63 - __clzll((long long)x);
+    b = 4 * (e - 1) + (int)((x >> (e - 2)) & 3u);
+  }
+  return b < nb - 1 ? b : nb - 1;
+}
+
+// sigma(x) = 1 / (1 + e^-x) = 1 / (1 + 2^(-x log2 e)) in fp32 on the
+// hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32).  Saturates cleanly:
+// 2^(+large) = inf gives 0, 2^(-large) = 0 gives 1.
+__device__ __forceinline__ float sigmoid_f(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -1.44269504088896341f));
+}
+
+}  // namespace hstu

@@ -1,0 +1,248 @@
+// LayerNorm + U-gating around the jagged attention, and the reduction of the
+// bias-table gradient partials.
+//
+//   forward   y = (o - mean) * rstd * u, per token over all H*d features,
+//             biased variance, rstd = 1/sqrt(var + eps); saves mean, rstd
+//   backward  du = n * dy;  g = dy * u;
+//             dO = rstd * (g - mean(g) - n * mean(g * n)),  n = (o - mean) * rstd
+//
+// One wave64 per token: each lane owns 8 consecutive features per 512-wide
+// chunk (one 16-byte bf16 load), statistics by wave shuffles.  These kernels
+// are HBM-bound (each feature is read and written once or twice).
+#include <algorithm>
+
+#include "internal.h"
+#include "device.h"
+
+namespace hstu {
+
+namespace {
+
+constexpr int LN_THREADS = 256;   // 4 tokens per work-group
+constexpr int LN_WAVES = LN_THREADS / 64;
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+template <typename T>
+struct Vec8;
+
+template <>
+struct Vec8<u16> {
+  __device__ static void load(const u16 *p, float (&f)[8]) {
+    const uint4 x = *(const uint4 *)p;
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = bf2f((u16)(w[e] & 0xffffu));
+      f[2 * e + 1] = bf2f((u16)(w[e] >> 16));
+    }
+  }
+  __device__ static void store(u16 *p, const float (&f)[8]) {
+    uint4 x;
+    x.x = pack2(f[0], f[1]);
+    x.y = pack2(f[2], f[3]);
+    x.z = pack2(f[4], f[5]);
+    x.w = pack2(f[6], f[7]);
+    *(uint4 *)p = x;
+  }
+};
+
+template <>
+struct Vec8<float> {
+  __device__ static void load(const float *p, float (&f)[8]) {
+    const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  __device__ static void store(float *p, const float (&f)[8]) {
+    *(float4 *)p = make_float4(f[0], f[1], f[2], f[3]);
+    *(float4 *)(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+  }
+};
+
+template <typename T>
+__global__ void __launch_bounds__(LN_THREADS)
+ln_fwd_kernel(const T *__restrict__ o, const T *__restrict__ u,
+              T *__restrict__ y, float *__restrict__ mean_out,
+              float *__restrict__ rstd_out, int64_t T_tokens, int F) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+  if (r >= T_tokens) return;
+  const T *orow = o + r * F;
+  float sum = 0.0f;
+  for (int f0 = lane * 8; f0 < F; f0 += 512) {
+    float z[8];
+    Vec8<T>::load(orow + f0, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sum += z[e];
+  }
+  const float mu = wave_sum(sum) / (float)F;
+  float sq = 0.0f;
+  for (int f0 = lane * 8; f0 < F; f0 += 512) {
+    float z[8];
+    Vec8<T>::load(orow + f0, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sq += (z[e] - mu) * (z[e] - mu);
+  }
+  const float rstd = rsqrtf(wave_sum(sq) / (float)F + HSTU_LN_EPS);
+  for (int f0 = lane * 8; f0 < F; f0 += 512) {
+    float z[8], uu[8], out[8];
+    Vec8<T>::load(orow + f0, z);
+    Vec8<T>::load(u + r * F + f0, uu);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = (z[e] - mu) * rstd * uu[e];
+    Vec8<T>::store(y + r * F + f0, out);
+  }
+  if (lane == 0) {
+    mean_out[r] = mu;
+    rstd_out[r] = rstd;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(LN_THREADS)
+ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
+              const T *__restrict__ o, const float *__restrict__ mean,
+              const float *__restrict__ rstd, T *__restrict__ du,
+              T *__restrict__ dO, float *__restrict__ dpos_part, int H,
+              int64_t T_tokens, int F) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+  if (r >= T_tokens) return;
+  const float mu = mean[r], rs = rstd[r];
+  const int64_t base = r * F;
+  float sg = 0.0f, sgn = 0.0f;
+  for (int f0 = lane * 8; f0 < F; f0 += 512) {
+    float z[8], g[8], uu[8];
+    Vec8<T>::load(o + base + f0, z);
+    Vec8<T>::load(dy + base + f0, g);
+    Vec8<T>::load(u + base + f0, uu);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float n = (z[e] - mu) * rs;
+      const float gg = g[e] * uu[e];
+      sg += gg;
+      sgn += gg * n;
+    }
+  }
+  const float mg = wave_sum(sg) / (float)F;
+  const float mgn = wave_sum(sgn) / (float)F;
+  for (int f0 = lane * 8; f0 < F; f0 += 512) {
+    float z[8], g[8], uu[8], o_du[8], o_do[8];
+    Vec8<T>::load(o + base + f0, z);
+    Vec8<T>::load(dy + base + f0, g);
+    Vec8<T>::load(u + base + f0, uu);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float n = (z[e] - mu) * rs;
+      o_du[e] = n * g[e];
+      o_do[e] = rs * (g[e] * uu[e] - mg - n * mgn);
+    }
+    Vec8<T>::store(du + base + f0, o_du);
+    Vec8<T>::store(dO + base + f0, o_do);
+  }
+  // the attention backward accumulates this token's d_pos partials
+  if (dpos_part && lane < H) dpos_part[r * H + lane] = 0.0f;
+}
+
+// d_pos[h, x]: x >= N is unreachable (j > i) and written 0; otherwise the
+// offset m = N-1-x sums the per-sequence partials of every sequence longer
+// than m.  d_time[h, k]: sum of the per-work-group histograms.
+constexpr int FIN_THREADS = 256;
+constexpr int FIN_SEQ_CHUNK = 1024;
+
+__global__ void __launch_bounds__(FIN_THREADS)
+finalize_pos_kernel(const SeqInfo *__restrict__ info, int B,
+                    const float *__restrict__ part, int H, int N,
+                    float *__restrict__ d_pos) {
+  __shared__ int64_t s_start[FIN_SEQ_CHUNK];
+  __shared__ int32_t s_len[FIN_SEQ_CHUNK];
+  const int64_t span = 2 * (int64_t)N - 1;
+  const int64_t idx = (int64_t)blockIdx.x * FIN_THREADS + threadIdx.x;
+  const bool active = idx < (int64_t)H * span;
+  const int h = active ? (int)(idx / span) : 0;
+  const int64_t x = active ? idx % span : 0;
+  const int64_t m = (int64_t)N - 1 - x;
+  float acc = 0.0f;
+  for (int b0 = 0; b0 < B; b0 += FIN_SEQ_CHUNK) {
+    const int nb = min(FIN_SEQ_CHUNK, B - b0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < nb; t += FIN_THREADS) {
+      s_start[t] = info[b0 + t].start;
+      s_len[t] = info[b0 + t].len;
+    }
+    __syncthreads();
+    if (active && m >= 0)
+      for (int t = 0; t < nb; ++t)
+        if (s_len[t] > m) acc += part[(s_start[t] + m) * H + h];
+  }
+  if (active) d_pos[idx] = acc;
+}
+
+__global__ void __launch_bounds__(FIN_THREADS)
+finalize_time_kernel(const float *__restrict__ part, int n_parts, int width,
+                     float *__restrict__ d_time) {
+  const int idx = blockIdx.x * FIN_THREADS + threadIdx.x;
+  if (idx >= width) return;
+  float acc = 0.0f;
+  for (int g = 0; g < n_parts; ++g) acc += part[(int64_t)g * width + idx];
+  d_time[idx] = acc;
+}
+
+}  // namespace
+
+hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
+                         void *y, float *mean, float *rstd, hipStream_t s) {
+  const int F = p.H * p.d;
+  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES));
+  if (p.dtype == HSTU_BF16)
+    hipLaunchKernelGGL(ln_fwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
+                       (const u16 *)o, (const u16 *)u, (u16 *)y, mean, rstd, p.T, F);
+  else
+    hipLaunchKernelGGL(ln_fwd_kernel<float>, grid, dim3(LN_THREADS), 0, s,
+                       (const float *)o, (const float *)u, (float *)y, mean, rstd, p.T, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_bwd(const Problem &p, const void *dy, const void *u,
+                         const void *o, const float *mean, const float *rstd,
+                         void *du, void *dO, float *dpos_part, hipStream_t s) {
+  const int F = p.H * p.d;
+  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES));
+  if (p.dtype == HSTU_BF16)
+    hipLaunchKernelGGL(ln_bwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
+                       (const u16 *)dy, (const u16 *)u, (const u16 *)o, mean, rstd,
+                       (u16 *)du, (u16 *)dO, dpos_part, p.H, p.T, F);
+  else
+    hipLaunchKernelGGL(ln_bwd_kernel<float>, grid, dim3(LN_THREADS), 0, s,
+                       (const float *)dy, (const float *)u, (const float *)o, mean, rstd,
+                       (float *)du, (float *)dO, dpos_part, p.H, p.T, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
+                                  float *d_time, hipStream_t s) {
+  const char *ws = (const char *)a.ws;
+  const Problem &p = a.p;
+  if (d_pos) {
+    const int64_t n = (int64_t)p.H * (2 * (int64_t)p.N - 1);
+    hipLaunchKernelGGL(finalize_pos_kernel, dim3((unsigned)((n + FIN_THREADS - 1) / FIN_THREADS)),
+                       dim3(FIN_THREADS), 0, s, (const SeqInfo *)(ws + a.L.seqinfo), p.B,
+                       (const float *)(ws + a.L.dpos_part), p.H, p.N, d_pos);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (d_time) {
+    const int width = p.H * p.nb;
+    hipLaunchKernelGGL(finalize_time_kernel, dim3((width + FIN_THREADS - 1) / FIN_THREADS),
+                       dim3(FIN_THREADS), 0, s, (const float *)(ws + a.L.dtime_part),
+                       a.L.dkv_grid, width, d_time);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace hstu

@@ -1,0 +1,264 @@
+"""Python binding of the jagged HSTU attention C ABI (include/hstu_jagged.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libhstu_jagged.so.  PyTorch supplies device memory and the
+current stream.  The functions with the C names take device tensors and
+write into caller-provided outputs; `forward` / `backward` are conveniences
+that allocate the outputs and the workspace with torch and then call them.
+
+If the shared library has not been built, every call raises: there is no
+fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhstu_jagged.so")
+
+HSTU_BF16, HSTU_F32 = 0, 1
+ERRORS = {-1: "HSTU_EINVAL", -2: "HSTU_ENOTSUP", -3: "HSTU_EWORKSPACE", -4: "HSTU_EHIP"}
+
+
+class HstuError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Rab(ctypes.Structure):
+    _fields_ = [("pos_w", ctypes.c_void_p), ("time_w", ctypes.c_void_p),
+                ("timestamps", ctypes.c_void_p), ("num_buckets", ctypes.c_int32)]
+
+
+class FwdOut(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("total_tokens", ctypes.c_int64),
+                ("y", ctypes.c_void_p), ("o", ctypes.c_void_p),
+                ("ln_mean", ctypes.c_void_p), ("ln_rstd", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class BwdIO(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("total_tokens", ctypes.c_int64),
+                ("dy", ctypes.c_void_p), ("o", ctypes.c_void_p),
+                ("ln_mean", ctypes.c_void_p), ("ln_rstd", ctypes.c_void_p),
+                ("dq", ctypes.c_void_p), ("dk", ctypes.c_void_p),
+                ("dv", ctypes.c_void_p), ("du", ctypes.c_void_p),
+                ("d_pos_w", ctypes.c_void_p), ("d_time_w", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libhstu_jagged.so; raises if it is missing (no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() "
+                          "(or python paper_2605_13433_amd/build.py) first")
+    lib = ctypes.CDLL(path)
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.hstu_jagged_attn_fwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32,
+                                         ctypes.POINTER(Rab), ctypes.POINTER(FwdOut), P]
+    lib.hstu_jagged_attn_fwd.restype = ctypes.c_int
+    lib.hstu_jagged_attn_bwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32,
+                                         ctypes.POINTER(Rab), ctypes.POINTER(BwdIO), P]
+    lib.hstu_jagged_attn_bwd.restype = ctypes.c_int
+    lib.hstu_jagged_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i64, i32,
+                                                     ctypes.c_int, ctypes.POINTER(Rab)]
+    lib.hstu_jagged_attn_workspace_bytes.restype = ctypes.c_size_t
+    lib.hstu_jagged_schedule.argtypes = [P, i32, i32, i64, P, P, P, P, ctypes.c_size_t, P]
+    lib.hstu_jagged_schedule.restype = ctypes.c_int
+    lib.hstu_last_error.argtypes = []
+    lib.hstu_last_error.restype = ctypes.c_char_p
+    lib.hstu_version.argtypes = []
+    lib.hstu_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().hstu_last_error().decode()
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the HIP library must be contiguous")
+    return t.data_ptr()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return HSTU_BF16
+    if t.dtype == torch.float32:
+        return HSTU_F32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def make_rab(pos_w=None, time_w=None, timestamps=None, num_buckets=128) -> Rab:
+    return Rab(_ptr(pos_w), _ptr(time_w), _ptr(timestamps),
+               int(num_buckets) if time_w is not None else 0)
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise HstuError(rc, last_error())
+
+
+def hstu_jagged_attn_workspace_bytes(B, max_len, H, d, total_tokens, for_bwd,
+                                     dtype_code, rab: Optional[Rab] = None) -> int:
+    n = load_library().hstu_jagged_attn_workspace_bytes(
+        int(B), int(max_len), int(H), int(d), int(total_tokens), int(for_bwd),
+        int(dtype_code), ctypes.byref(rab) if rab is not None else None)
+    if n == 0:
+        raise HstuError(-1, last_error())
+    return n
+
+
+def hstu_jagged_attn_fwd(q, k, v, u, seq_offsets, B, max_len, H, d,
+                         rab: Optional[Rab], out: FwdOut, stream=None) -> None:
+    _check(load_library().hstu_jagged_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(seq_offsets), int(B),
+        int(max_len), int(H), int(d), ctypes.byref(rab) if rab is not None else None,
+        ctypes.byref(out), _stream(stream)))
+
+
+def hstu_jagged_attn_bwd(q, k, v, u, seq_offsets, B, max_len, H, d,
+                         rab: Optional[Rab], io: BwdIO, stream=None) -> None:
+    _check(load_library().hstu_jagged_attn_bwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(seq_offsets), int(B),
+        int(max_len), int(H), int(d), ctypes.byref(rab) if rab is not None else None,
+        ctypes.byref(io), _stream(stream)))
+
+
+def hstu_jagged_schedule(seq_offsets, B, max_len, total_tokens, n_entries, list_q,
+                         list_k, workspace, stream=None) -> None:
+    _check(load_library().hstu_jagged_schedule(
+        _ptr(seq_offsets), int(B), int(max_len), int(total_tokens), _ptr(n_entries),
+        _ptr(list_q), _ptr(list_k), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def max_entries(B: int, max_len: int, total_tokens: int) -> int:
+    """Capacity of a work list: min(B*ceil(N/64), (T + 63B)/64)."""
+    return min(B * ((max_len + 63) // 64), (total_tokens + 63 * B) // 64)
+
+
+def schedule(seq_offsets, max_len, total_tokens):
+    """Runs the device scheduler; returns (q_list, k_list) as int32 [E, 2] CPU tensors."""
+    B = seq_offsets.numel() - 1
+    dev = seq_offsets.device
+    cap = max(max_entries(B, max_len, total_tokens), 1)
+    ws = _workspace(hstu_jagged_attn_workspace_bytes(B, max_len, 1, 64, total_tokens, 1,
+                                                     HSTU_F32, None), dev)
+    n = torch.zeros(1, dtype=torch.int32, device=dev)
+    lq = torch.full((cap, 2), -1, dtype=torch.int32, device=dev)
+    lk = torch.full((cap, 2), -1, dtype=torch.int32, device=dev)
+    hstu_jagged_schedule(seq_offsets, B, max_len, total_tokens, n, lq, lk, ws)
+    E = int(n.item())
+    return lq[:E].cpu(), lk[:E].cpu()
+
+
+# ---------------------------------------------------------------- helpers
+@dataclass
+class FwdResult:
+    y: torch.Tensor
+    o: torch.Tensor
+    ln_mean: torch.Tensor
+    ln_rstd: torch.Tensor
+
+
+@dataclass
+class BwdResult:
+    dq: torch.Tensor
+    dk: torch.Tensor
+    dv: torch.Tensor
+    du: torch.Tensor
+    d_pos_w: Optional[torch.Tensor]
+    d_time_w: Optional[torch.Tensor]
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+class Plan:
+    """Outputs + workspace for one problem shape, allocated once and reused."""
+
+    def __init__(self, q, seq_offsets, max_len, pos_w=None, time_w=None,
+                 timestamps=None, num_buckets=128, backward=True):
+        T, H, d = q.shape
+        dev = q.device
+        self.B = seq_offsets.numel() - 1
+        self.N, self.H, self.d, self.T = int(max_len), H, d, T
+        self.rab = make_rab(pos_w, time_w, timestamps, num_buckets)
+        self._keep = (pos_w, time_w, timestamps)
+        code = _dtype_code(q)
+        self.fwd_ws = _workspace(hstu_jagged_attn_workspace_bytes(
+            self.B, self.N, H, d, T, 0, code, self.rab), dev)
+        self.y = torch.empty(T, H * d, dtype=q.dtype, device=dev)
+        self.o = torch.empty(T, H, d, dtype=q.dtype, device=dev)
+        self.mean = torch.empty(T, dtype=torch.float32, device=dev)
+        self.rstd = torch.empty(T, dtype=torch.float32, device=dev)
+        self.out = FwdOut(code, T, _ptr(self.y), _ptr(self.o), _ptr(self.mean),
+                          _ptr(self.rstd), _ptr(self.fwd_ws), self.fwd_ws.numel())
+        self.io = None
+        if backward:
+            self.bwd_ws = _workspace(hstu_jagged_attn_workspace_bytes(
+                self.B, self.N, H, d, T, 1, code, self.rab), dev)
+            self.dq = torch.empty(T, H, d, dtype=q.dtype, device=dev)
+            self.dk = torch.empty_like(self.dq)
+            self.dv = torch.empty_like(self.dq)
+            self.du = torch.empty(T, H * d, dtype=q.dtype, device=dev)
+            self.d_pos = (torch.empty(H, 2 * self.N - 1, dtype=torch.float32, device=dev)
+                          if pos_w is not None else None)
+            self.d_time = (torch.empty(H, num_buckets, dtype=torch.float32, device=dev)
+                           if time_w is not None else None)
+            self.io = BwdIO(code, T, None, _ptr(self.o), _ptr(self.mean), _ptr(self.rstd),
+                            _ptr(self.dq), _ptr(self.dk), _ptr(self.dv), _ptr(self.du),
+                            _ptr(self.d_pos), _ptr(self.d_time), _ptr(self.bwd_ws),
+                            self.bwd_ws.numel())
+
+    def forward(self, q, k, v, u, seq_offsets, stream=None) -> FwdResult:
+        hstu_jagged_attn_fwd(q, k, v, u, seq_offsets, self.B, self.N, self.H, self.d,
+                             self.rab, self.out, stream)
+        return FwdResult(self.y, self.o, self.mean, self.rstd)
+
+    def backward(self, q, k, v, u, seq_offsets, dy, stream=None) -> BwdResult:
+        self.io.dy = _ptr(dy)
+        self._dy = dy
+        hstu_jagged_attn_bwd(q, k, v, u, seq_offsets, self.B, self.N, self.H, self.d,
+                             self.rab, self.io, stream)
+        return BwdResult(self.dq, self.dk, self.dv, self.du, self.d_pos, self.d_time)
+
+
+def forward(q, k, v, u, seq_offsets, max_len, pos_w=None, time_w=None,
+            timestamps=None, num_buckets=128) -> FwdResult:
+    plan = Plan(q, seq_offsets, max_len, pos_w, time_w, timestamps, num_buckets,
+                backward=False)
+    return plan.forward(q, k, v, u, seq_offsets)
+
+
+def forward_backward(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=None,
+                     timestamps=None, num_buckets=128):
+    plan = Plan(q, seq_offsets, max_len, pos_w, time_w, timestamps, num_buckets)
+    f = plan.forward(q, k, v, u, seq_offsets)
+    g = plan.backward(q, k, v, u, seq_offsets, dy)
+    return f, g

@@ -1,0 +1,203 @@
+"""GPU parity: the HIP path against the CPU oracle, element by element.
+
+Tolerance per output tensor: max|gpu - ref| <= 2e-2 max|ref| for bf16 and
+1e-5 max|ref| for fp32, on y, o, dq, dk, dv, du, d_pos and d_time (o is
+checked as well as y: LayerNorm is scale-invariant, so a wrong global scale
+of o would hide in y).  Small cases span several 64-row tiles, ragged tails,
+empty and single-token sequences and L = max_len; the five workloads run at
+full size in the launch configuration the benchmark times, with the oracle
+on every row for the small ones and on sampled whole sequences for the
+large ones.  Sequence handling (offsets, masks, isolation) is checked
+bit-exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2605_13433_amd import inputs
+from tests.gpu_util import TOL, check, rows_of, run_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.build(force=False)
+
+
+def compare(w, got, ref_f, ref_b=None, rows=None, tables=True):
+    tol = TOL[w.dtype]
+    sel = (lambda a: a) if rows is None else (lambda a: a[rows])
+    check("o", sel(got["o"]), ref_f["o"], tol)
+    check("y", sel(got["y"]), ref_f["y"], tol)
+    if ref_b is not None:
+        for n in ("dq", "dk", "dv", "du"):
+            check(n, sel(got[n]), ref_b[n], tol)
+        if tables and w.pos_w is not None:
+            check("d_pos", got["d_pos"], ref_b["d_pos"], tol)
+        if tables and w.time_w is not None:
+            check("d_time", got["d_time"], ref_b["d_time"], tol)
+
+
+SMALL = [
+    # lengths, H, d, N, pos, time
+    ([1, 63, 64, 65, 130, 0, 200, 17, 256], 2, 64, 256, True, True),
+    ([1, 63, 64, 65, 130, 0, 200, 17, 256], 2, 128, 256, True, True),
+    ([129, 5, 64, 191], 3, 64, 192, True, False),
+    ([100, 33, 0, 7], 1, 128, 128, False, True),
+    ([77, 250, 3], 2, 64, 250, False, False),
+    ([2, 1, 1, 3, 64], 4, 64, 64, True, True),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_bf16(case):
+    lengths, H, d, N, pos, time = SMALL[case]
+    say(f"small bf16 case {case}: lengths={lengths} H={H} d={d} N={N} pos={pos} time={time}")
+    w = inputs.make_workload(lengths, H=H, d=d, N=N, pos=pos, time=time, seed=100 + case)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_small_f32(d):
+    lengths = [1, 70, 0, 33, 128]
+    say(f"small fp32 d={d}: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=2, d=d, N=128, dtype=torch.float32, seed=200 + d)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def test_workload1_fp32_forward():
+    w = inputs.workload(1)
+    say(f"workload 1 {w.name}: T={w.T} pairs/head={w.pairs}")
+    got = run_gpu(w, bwd=False)
+    compare(w, got, oracle.fwd_workload(w))
+
+
+def test_workload2_full():
+    w = inputs.workload(2)
+    say(f"workload 2 {w.name}: T={w.T} pairs/head={w.pairs}")
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def _sampled(index, picks, max_pairs):
+    """Full-size GPU run; oracle on sampled whole sequences.  Table
+    gradients sum over every sequence, so they are checked on the sampled
+    sub-batch run by itself, and the full batch's tables must equal the sum
+    of the sample's and the complement's (additivity over sequences)."""
+    w = inputs.workload(index)
+    say(f"workload {index} {w.name}: T={w.T} pairs/head={w.pairs} (full-size GPU run)")
+    got = run_gpu(w)
+    L = w.lengths
+    order = np.argsort(L)
+    rng = np.random.default_rng(index)
+    chosen = set(int(b) for b in order[:2])                     # shortest
+    fits = [int(b) for b in order if L[b] * (L[b] + 1) // 2 <= max_pairs]
+    chosen.add(fits[-1])                                        # longest that fits
+    chosen |= set(int(b) for b in rng.choice(fits, size=picks, replace=False))
+    seqs = sorted(chosen)
+    sub = inputs.subset(w, seqs)
+    say(f"  sampled sequences {seqs} lengths {L[seqs].tolist()}")
+    ref_f = oracle.fwd_workload(sub)
+    ref_b = oracle.bwd_workload(sub)
+    rows = rows_of(w, seqs)
+    compare(w, got, ref_f, ref_b, rows=rows, tables=False)
+    say("  tables on the sampled sub-batch:")
+    got_sub = run_gpu(sub)
+    compare(sub, got_sub, ref_f, ref_b)
+    rest = [b for b in range(w.B) if b not in chosen]
+    got_rest = run_gpu(inputs.subset(w, rest))
+    for n in ("d_pos", "d_time"):
+        if got[n] is not None:
+            check(n + "+", got_sub[n] + got_rest[n], got[n], 1e-3)
+
+
+def test_workload3_sampled():
+    _sampled(3, picks=5, max_pairs=1_200_000)
+
+
+def test_workload4_attention_sampled():
+    _sampled(4, picks=3, max_pairs=1_500_000)
+
+
+def test_workload5_sampled():
+    _sampled(5, picks=8, max_pairs=2_000_000)
+
+
+# ---------------------------------------------------- bit-exact jagged handling
+def _fwd_bits(w):
+    got = run_gpu(w, bwd=False)
+    return got["o"], got["y"]
+
+
+def test_causality_and_isolation_bitwise():
+    lengths = [150, 70, 129]
+    w = inputs.make_workload(lengths, H=2, d=64, N=256, seed=7)
+    say("bitwise causality / isolation, lengths=" + str(lengths))
+    o0, y0 = _fwd_bits(w)
+    t = 40                       # perturb token 40 of sequence 0 (and later ones)
+    for name in ("q", "k", "v", "u"):
+        x = getattr(w, name).clone()
+        x[t] += 1.0
+        old = getattr(w, name)
+        setattr(w, name, x)
+        o1, y1 = _fwd_bits(w)
+        setattr(w, name, old)
+        assert np.array_equal(o1[:t], o0[:t]) and np.array_equal(y1[:t], y0[:t]), name
+        assert np.array_equal(o1[150:], o0[150:]) and np.array_equal(y1[150:], y0[150:]), name
+    ts = w.timestamps.clone()
+    ts[t:150] += 5000
+    old = w.timestamps
+    w.timestamps = ts
+    o1, _ = _fwd_bits(w)
+    w.timestamps = old
+    assert np.array_equal(o1[:t], o0[:t]) and np.array_equal(o1[150:], o0[150:])
+
+
+def test_split_and_permute_bitwise():
+    lengths = [65, 1, 200, 0, 64, 33]
+    w = inputs.make_workload(lengths, H=2, d=128, N=256, seed=8)
+    say("bitwise split / permutation, lengths=" + str(lengths))
+    o0, y0 = _fwd_bits(w)
+    off = w.seq_offsets.numpy()
+    for part in ([0, 1, 2], [3, 4, 5], [5, 2, 0, 4, 1, 3]):
+        sub = inputs.subset(w, part)
+        o1, y1 = _fwd_bits(sub)
+        rows = np.concatenate([np.arange(off[b], off[b + 1]) for b in part]).astype(int)
+        assert np.array_equal(o1, o0[rows]) and np.array_equal(y1, y0[rows]), part
+
+
+def test_forward_deterministic_and_guard_bands():
+    from paper_2605_13433_amd import hstu
+    w = inputs.make_workload([100, 64, 3], H=2, d=64, N=128, seed=9)
+    say("determinism + guard bands")
+    dev = lambda t: t.contiguous().cuda()
+    q, k, v, u, off = (dev(x) for x in (w.q, w.k, w.v, w.u, w.seq_offsets))
+    pos, tw, ts = dev(w.pos_w), dev(w.time_w), dev(w.timestamps)
+    plan = hstu.Plan(q, off, w.N, pos, tw, ts, w.num_buckets, backward=False)
+    T, H, d = q.shape
+    pad = 4096
+    canary = torch.full((T * H * d + 2 * pad,), -12345.0, dtype=torch.bfloat16, device="cuda")
+    o_view = canary[pad:pad + T * H * d].view(T, H, d)
+    plan.o = o_view
+    plan.out.o = o_view.data_ptr()
+    r1 = plan.forward(q, k, v, u, off).y.clone()
+    r2 = plan.forward(q, k, v, u, off).y.clone()
+    torch.cuda.synchronize()
+    assert torch.equal(r1, r2)
+    assert torch.all(canary[:pad] == -12345.0) and torch.all(canary[pad + T * H * d:] == -12345.0)
+
+
+def test_degenerate_batches():
+    say("degenerate: all-empty batch backward writes zero tables; L = N; B = 1")
+    w = inputs.make_workload([0, 0, 0], H=2, d=64, N=64, seed=10)
+    got = run_gpu(w)
+    assert np.all(got["d_pos"] == 0) and np.all(got["d_time"] == 0)
+    w = inputs.make_workload([64], H=1, d=64, N=64, seed=11)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
