@@ -1,0 +1,315 @@
+"""Benchmark: jagged HSTU attention forward + backward on one MI355X.
+
+One step = the whole hot path over one batch: the forward call (scheduler,
+attention, LayerNorm x U) and the backward call (scheduler, LayerNorm
+backward, dQ, dK/dV with table gradients, table finalize), on synthetic
+inputs already resident in HBM.
+
+Headline: valid-token TFLOP/s = 12 d H P / t_step, with P = sum_b
+L_b (L_b + 1) / 2 causal pairs per head (forward 4 d H P for QK^T and AV,
+backward 8 d H P for dA, dV, dQ, dK; recompute, bias, SiLU and LayerNorm
+work are not credited; padding does not exist).  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3           # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # flop per byte
+
+KERNEL_SOURCES = ["device.h", "internal.h", "sched.hip", "attn_bf16.hip",
+                  "attn_f32.hip", "norm.hip", "api.cpp"]
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2605_13433_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_work(name, w, elem_bytes):
+    """(algorithmic bytes, algorithmic flops) of one launch of `name`.
+
+    Bytes count each tensor element read or written once at its storage
+    width, per (token, head, dim) element E = T*H*d:
+      attn_fwd   reads q, k, v; writes o                    4 E elements
+      ln_fwd     reads o, u; writes y  (+ mean, rstd)       3 E (+ 2 T fp32)
+      ln_bwd     reads dy, u, o; writes du, dO (+ stats)    5 E (+ 2 T fp32)
+      attn_dq    reads q, k, v, dO; writes dq               5 E
+      attn_dkv   reads q, k, v, dO; writes dk, dv           6 E
+    Flops are the credited contractions: fwd QK^T + AV = 4 d H P; dQ kernel
+    dA + dQ = 4 d H P; dK/dV kernel dV + dK = 4 d H P.
+    """
+    E = w.T * w.H * w.d
+    P = w.pairs
+    tok = 8 * w.T
+    table = {
+        "attn_fwd": (4 * E * elem_bytes, 4 * w.d * w.H * P),
+        "ln_fwd": (3 * E * elem_bytes + tok, 0),
+        "ln_bwd": (5 * E * elem_bytes + tok, 0),
+        "attn_dq": (5 * E * elem_bytes, 4 * w.d * w.H * P),
+        "attn_dkv": (6 * E * elem_bytes, 4 * w.d * w.H * P),
+    }
+    return table.get(name, (0, 0))
+
+
+def load_traffic(kernel: str, workload: str, sha: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha") != sha:
+        return None
+    try:
+        fetch = float(vals["fetch_kib_per_dispatch"])
+        write = float(vals["write_kib_per_dispatch"])
+        scale_f = float(vals.get("fetch_scale", 1.0))
+        scale_w = float(vals.get("write_scale", 1.0))
+    except (KeyError, ValueError):
+        return None
+    return (fetch * scale_f + write * scale_w) * 1024.0
+
+
+def cpu_baseline(w, target_s=12.0):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    whole sequences in a seeded random order until the estimated
+    forward+backward time reaches `target_s`."""
+    from oracle import oracle
+    from paper_2605_13433_amd import inputs
+    oracle.build(force=False)
+    rng = np.random.default_rng(12345)
+    order = rng.permutation(w.B)
+    # calibrate on a small slice, then size the sample
+    pairs = w.lengths * (w.lengths + 1) // 2
+    probe, acc = [], 0
+    for b in order:
+        probe.append(int(b))
+        acc += pairs[b]
+        if acc >= 2e5:
+            break
+    sub = inputs.subset(w, sorted(probe))
+    t0 = time.perf_counter()
+    oracle.fwd_workload(sub)
+    oracle.bwd_workload(sub)
+    rate = max(acc, 1) / max(time.perf_counter() - t0, 1e-6)   # pairs per second
+    budget = rate * target_s
+    seqs, acc = [], 0
+    for b in order:
+        if acc + pairs[b] > budget and seqs:
+            continue
+        seqs.append(int(b))
+        acc += pairs[b]
+    sub = inputs.subset(w, sorted(seqs))
+    t0 = time.perf_counter()
+    oracle.fwd_workload(sub)
+    oracle.bwd_workload(sub)
+    dt = time.perf_counter() - t0
+    flops = 12.0 * w.d * w.H * sub.pairs
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"{len(seqs)} of {w.B} sequences ({sub.T} tokens, {sub.pairs} "
+                   f"causal pairs/head, {100.0 * sub.pairs / w.pairs:.1f}% of the "
+                   f"batch's pairs), f64 forward + backward, {dt:.1f} s"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="extra steps, each after a 1 GiB cache flush")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run 5 device copies of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.copy_probe_mib:
+        import torch
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": src.numel() * 4}))
+        return
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the jagged attention "
+              "on a single MI355X (sequences shard across GPUs without any exchange "
+              "in the forward; see the design notes). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_13433_amd import hstu, inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    lib = hstu.load_library()
+
+    w = inputs.workload(args.workload, args.seed)
+    if w.dy is None:
+        print(f"workload {args.workload} is forward-only; pick a fwd+bwd workload",
+              file=sys.stderr)
+        sys.exit(2)
+    dev = lambda t: None if t is None else t.contiguous().cuda()
+    q, k, v, u, off = (dev(x) for x in (w.q, w.k, w.v, w.u, w.seq_offsets))
+    dy = dev(w.dy)
+    pos, tw, ts = dev(w.pos_w), dev(w.time_w), dev(w.timestamps)
+    plan = hstu.Plan(q, off, w.N, pos, tw, ts, w.num_buckets, backward=True)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        plan.forward(q, k, v, u, off, stream)
+        plan.backward(q, k, v, u, off, dy, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    flops_step = 12.0 * w.d * w.H * w.pairs
+    value = flops_step / (ms_per_step * 1e-3) / 1e12
+
+    # ---- per-kernel durations: HIP events around every launch, same stream
+    import ctypes
+    lib.hstu_profile_enable(1)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    lib.hstu_profile_enable(0)
+    nmax = 32
+    names = (ctypes.c_char_p * nmax)()
+    tot = (ctypes.c_double * nmax)()
+    cnt = (ctypes.c_int * nmax)()
+    lib.hstu_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
+                                      ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_int)]
+    rows = lib.hstu_profile_read(nmax, names, tot, cnt)
+    kernels = {}
+    for i in range(max(rows, 0)):
+        kernels[names[i].decode()] = {"avg_us": 1e3 * tot[i] / cnt[i], "launches": cnt[i]}
+
+    # ---- cold cache: flush L2 + MALL (1 GiB of writes) before each step
+    cold_ms = None
+    if args.cold_steps > 0:
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        times = []
+        for _ in range(args.cold_steps):
+            flush.fill_(1.0)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            step()
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        cold_ms = float(np.median(times))
+        del flush
+
+    # ---- roofline of the dominant kernel
+    elem_bytes = 2 if w.dtype == torch.bfloat16 else 4
+    sha = kernel_source_sha()
+    per_kernel_total = {n: r["avg_us"] * r["launches"] for n, r in kernels.items()}
+    dominant = max(per_kernel_total, key=per_kernel_total.get)
+    nbytes, nflops = kernel_work(dominant, w, elem_bytes)
+    avg_s = kernels[dominant]["avg_us"] * 1e-6
+    if nflops and nbytes and nflops / nbytes > RIDGE:
+        roof = {"bound": "mfma", "achieved": nflops / avg_s / 1e12,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": nbytes / avg_s / 1e9,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = dominant
+    traffic = load_traffic(dominant, w.name, sha)
+    roof["traffic"] = traffic
+    roof["algorithmic_bytes"] = nbytes
+    roof["algorithmic_flops"] = nflops
+
+    for n, r in kernels.items():
+        b, f = kernel_work(n, w, elem_bytes)
+        s = r["avg_us"] * 1e-6
+        r["GB_s"] = round(b / s / 1e9, 1) if b else None
+        r["TFLOP_s"] = round(f / s / 1e12, 2) if f else None
+        r["avg_us"] = round(r["avg_us"], 2)
+
+    out = {
+        "metric": "jagged HSTU attn fwd+bwd valid-token TFLOP/s + % of bf16 MFMA peak, 1 GPU",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
+        "data": "synthetic (seeded long-tailed jagged lengths, N(0,1) q/k/v/u/dy, "
+                "N(0,0.1) bias tables, Poisson-gap timestamps)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "d": w.d, "max_len": w.N,
+                   "total_tokens": w.T, "causal_pairs_per_head": w.pairs,
+                   "max_seq_len": int(w.lengths.max()), "rab": {
+                       "pos": w.pos_w is not None, "time": w.time_w is not None,
+                       "num_buckets": w.num_buckets if w.time_w is not None else 0},
+                   "seed": args.workload if args.seed is None else args.seed,
+                   "parallelism": "single GPU"},
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 3),
+        "wall_s_timed_region": round(wall_s, 4),
+        "cold_ms_per_step": None if cold_ms is None else round(cold_ms, 5),
+        "cold_value": None if cold_ms is None else round(flops_step / (cold_ms * 1e-3) / 1e12, 3),
+        "kernels": kernels,
+        "roofline": roof,
+        "kernel_source_sha": sha,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -155,6 +155,17 @@ int hstu_jagged_schedule(const int64_t *seq_offsets, int32_t B,
                          int32_t *n_entries, int32_t *list_q, int32_t *list_k,
                          void *workspace, size_t workspace_bytes, void *stream);
 
+/* Diagnostics: per-kernel timing.  While enabled, every kernel the library
+ * launches is bracketed by two HIP events recorded on the stream it is
+ * launched on (the caller's stream).  hstu_profile_read waits for the
+ * recorded events, fills up to `max` rows (kernel name -- a static string
+ * owned by the library --, summed milliseconds, launch count) and clears
+ * the records; it returns the number of rows written or a negative code.
+ * Host-side only: no device memory is allocated. */
+int hstu_profile_enable(int on);
+int hstu_profile_read(int max, const char **names, double *total_ms,
+                      int *launches);
+
 /* Thread-local description of the last failure ("" if none). */
 const char *hstu_last_error(void);
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -63,7 +64,7 @@ int validate(const void *q, const void *k, const void *v, const void *u,
   const bool has_time = rab && rab->time_w;
   int32_t nb = 0;
   if (has_time) {
-    if (!rab->timestamps)
+    if (!rab->timestamps && T > 0)
       return fail(HSTU_EINVAL, "rab->time_w given without rab->timestamps");
     if (rab->num_buckets < 1)
       return fail(HSTU_EINVAL, "rab->num_buckets = %d < 1", rab->num_buckets);
@@ -94,6 +95,55 @@ int current_device(int *dev) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   return HSTU_OK;
 }
+
+// Optional per-kernel timing: events recorded around each launch on the
+// launch stream (see hstu_profile_enable).
+namespace prof {
+struct Rec {
+  const char *name;
+  hipEvent_t a, b;
+};
+std::atomic<bool> on{false};
+std::mutex mu;
+std::vector<Rec> recs;
+std::vector<hipEvent_t> pool;
+
+hipEvent_t take_event() {
+  if (!pool.empty()) {
+    hipEvent_t e = pool.back();
+    pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
+
+struct Scope {
+  const char *name;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  Scope(const char *n, hipStream_t st) : name(n), s(st) {
+    if (!on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lock(mu);
+    a = take_event();
+    if (a && hipEventRecord(a, s) != hipSuccess) {
+      pool.push_back(a);
+      a = nullptr;
+    }
+  }
+  ~Scope() {
+    if (!a) return;
+    std::lock_guard<std::mutex> lock(mu);
+    hipEvent_t b = take_event();
+    if (b && hipEventRecord(b, s) == hipSuccess) {
+      recs.push_back(Rec{name, a, b});
+    } else {
+      pool.push_back(a);
+      if (b) pool.push_back(b);
+    }
+  }
+};
+}  // namespace prof
 
 }  // namespace
 
@@ -221,12 +271,22 @@ int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
              p.has_time ? rab->time_w : nullptr,
              p.has_time ? rab->timestamps : nullptr,
              out->workspace, L, p};
-  hipError_t e = launch_schedule(seq_offsets, p, out->workspace, L, s);
+  hipError_t e;
+  {
+    prof::Scope ps("schedule", s);
+    e = launch_schedule(seq_offsets, p, out->workspace, L, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "schedule launch");
-  e = p.dtype == HSTU_BF16 ? launch_attn_fwd_bf16(a, out->o, s)
-                           : launch_attn_fwd_f32(a, out->o, s);
+  {
+    prof::Scope ps(p.dtype == HSTU_BF16 ? "attn_fwd" : "attn_fwd_f32", s);
+    e = p.dtype == HSTU_BF16 ? launch_attn_fwd_bf16(a, out->o, s)
+                             : launch_attn_fwd_f32(a, out->o, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "attention forward launch");
-  e = launch_ln_fwd(p, out->o, u, out->y, out->ln_mean, out->ln_rstd, s);
+  {
+    prof::Scope ps("ln_fwd", s);
+    e = launch_ln_fwd(p, out->o, u, out->y, out->ln_mean, out->ln_rstd, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "layernorm forward launch");
   return HSTU_OK;
 }
@@ -263,27 +323,78 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
   char *ws = (char *)io->workspace;
   float *d_pos = p.has_pos ? io->d_pos_w : nullptr;
   float *d_time = p.has_time ? io->d_time_w : nullptr;
-  hipError_t e = launch_schedule(seq_offsets, p, ws, L, s);
+  hipError_t e;
+  {
+    prof::Scope ps("schedule", s);
+    e = launch_schedule(seq_offsets, p, ws, L, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "schedule launch");
   if (p.T > 0) {
+    prof::Scope ps("ln_bwd", s);
     e = launch_ln_bwd(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
                       ws + L.dO, L.dpos_part ? (float *)(ws + L.dpos_part) : nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
   }
   if (p.dtype == HSTU_BF16) {
     if (p.T > 0) {
+      prof::Scope ps("attn_dq", s);
       e = launch_attn_dq_bf16(a, ws + L.dO, io->dq, s);
       if (e != hipSuccess) return hip_fail(e, "attention dQ launch");
     }
-    e = launch_attn_dkv_bf16(a, ws + L.dO, io->dk, io->dv, s);
+    {
+      prof::Scope ps("attn_dkv", s);
+      e = launch_attn_dkv_bf16(a, ws + L.dO, io->dk, io->dv, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "attention dK/dV launch");
-    e = launch_finalize_tables(a, d_pos, d_time, s);
+    {
+      prof::Scope ps("finalize_tables", s);
+      e = launch_finalize_tables(a, d_pos, d_time, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "table finalize launch");
   } else {
+    prof::Scope ps("attn_bwd_f32", s);
     e = launch_attn_bwd_f32(a, ws + L.dO, io->dq, io->dk, io->dv, d_pos, d_time, s);
     if (e != hipSuccess) return hip_fail(e, "attention backward launch");
   }
   return HSTU_OK;
+}
+
+int hstu_profile_enable(int on) {
+  prof::on.store(on != 0);
+  return HSTU_OK;
+}
+
+int hstu_profile_read(int max, const char **names, double *total_ms,
+                      int *launches) {
+  g_last_error.clear();
+  if (max < 0 || (max > 0 && (!names || !total_ms || !launches)))
+    return fail(HSTU_EINVAL, "bad profile_read arguments");
+  std::lock_guard<std::mutex> lock(prof::mu);
+  int rows = 0;
+  int rc = 0;
+  for (const prof::Rec &r : prof::recs) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) rc = hip_fail(e, "profile event");
+    int k = 0;
+    while (k < rows && std::strcmp(names[k], r.name) != 0) ++k;
+    if (k == rows) {
+      if (rows == max) continue;
+      names[k] = r.name;
+      total_ms[k] = 0.0;
+      launches[k] = 0;
+      ++rows;
+    }
+    total_ms[k] += ms;
+    launches[k] += 1;
+  }
+  for (const prof::Rec &r : prof::recs) {
+    prof::pool.push_back(r.a);
+    prof::pool.push_back(r.b);
+  }
+  prof::recs.clear();
+  return rc < 0 ? rc : rows;
 }
 
 }  // extern "C"

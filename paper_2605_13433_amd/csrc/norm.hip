@@ -149,48 +149,58 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
   if (dpos_part && lane < H) dpos_part[r * H + lane] = 0.0f;
 }
 
-// d_pos[h, x]: x >= N is unreachable (j > i) and written 0; otherwise the
-// offset m = N-1-x sums the per-sequence partials of every sequence longer
-// than m.  d_time[h, k]: sum of the per-work-group histograms.
-constexpr int FIN_THREADS = 256;
-constexpr int FIN_SEQ_CHUNK = 1024;
+// Table-gradient finalize, one launch with two block roles:
+//   d_pos[h, x]: x >= N is unreachable (j > i) and written 0; otherwise the
+//     offset m = N-1-x sums the per-sequence partials of every sequence
+//     longer than m.  Block = (h, 64 consecutive m); lane = m, waves stride
+//     over the sequences, then a cross-wave sum in LDS.
+//   d_time[h, k]: sum over work-groups of the dK/dV kernel's histograms.
+//     Block = 64 consecutive (h, k) columns; waves stride over the partials.
+// Summation order is fixed, so the result is deterministic given the
+// partials.
+constexpr int FIN_THREADS = 512;
+constexpr int FIN_WAVES = FIN_THREADS / 64;
 
 __global__ void __launch_bounds__(FIN_THREADS)
-finalize_pos_kernel(const SeqInfo *__restrict__ info, int B,
-                    const float *__restrict__ part, int H, int N,
-                    float *__restrict__ d_pos) {
-  __shared__ int64_t s_start[FIN_SEQ_CHUNK];
-  __shared__ int32_t s_len[FIN_SEQ_CHUNK];
-  const int64_t span = 2 * (int64_t)N - 1;
-  const int64_t idx = (int64_t)blockIdx.x * FIN_THREADS + threadIdx.x;
-  const bool active = idx < (int64_t)H * span;
-  const int h = active ? (int)(idx / span) : 0;
-  const int64_t x = active ? idx % span : 0;
-  const int64_t m = (int64_t)N - 1 - x;
+finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
+                       const float *__restrict__ pos_part, int H, int N,
+                       float *__restrict__ d_pos, int pos_blocks,
+                       const float *__restrict__ time_part, int n_parts,
+                       int width, float *__restrict__ d_time) {
+  __shared__ float red[FIN_WAVES][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   float acc = 0.0f;
-  for (int b0 = 0; b0 < B; b0 += FIN_SEQ_CHUNK) {
-    const int nb = min(FIN_SEQ_CHUNK, B - b0);
-    __syncthreads();
-    for (int t = threadIdx.x; t < nb; t += FIN_THREADS) {
-      s_start[t] = info[b0 + t].start;
-      s_len[t] = info[b0 + t].len;
+  if ((int)blockIdx.x < pos_blocks) {
+    const int chunks = (N + 63) / 64;
+    const int h = blockIdx.x / chunks;
+    const int m = (blockIdx.x % chunks) * 64 + lane;
+    if (m < N) {
+      for (int b = wv; b < B; b += FIN_WAVES) {
+        const SeqInfo si = info[b];
+        if (si.len > m) acc += pos_part[(si.start + m) * H + h];
+      }
     }
+    red[wv][lane] = acc;
     __syncthreads();
-    if (active && m >= 0)
-      for (int t = 0; t < nb; ++t)
-        if (s_len[t] > m) acc += part[(s_start[t] + m) * H + h];
+    if (wv == 0 && m < N) {
+      float s = 0.0f;
+      for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
+      const int64_t span = 2 * (int64_t)N - 1;
+      d_pos[h * span + (N - 1 - m)] = s;
+      if (N + m < span) d_pos[h * span + N + m] = 0.0f;
+    }
+  } else {
+    const int c = ((int)blockIdx.x - pos_blocks) * 64 + lane;
+    if (c < width)
+      for (int g = wv; g < n_parts; g += FIN_WAVES) acc += time_part[(int64_t)g * width + c];
+    red[wv][lane] = acc;
+    __syncthreads();
+    if (wv == 0 && c < width) {
+      float s = 0.0f;
+      for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
+      d_time[c] = s;
+    }
   }
-  if (active) d_pos[idx] = acc;
-}
-
-__global__ void __launch_bounds__(FIN_THREADS)
-finalize_time_kernel(const float *__restrict__ part, int n_parts, int width,
-                     float *__restrict__ d_time) {
-  const int idx = blockIdx.x * FIN_THREADS + threadIdx.x;
-  if (idx >= width) return;
-  float acc = 0.0f;
-  for (int g = 0; g < n_parts; ++g) acc += part[(int64_t)g * width + idx];
-  d_time[idx] = acc;
 }
 
 }  // namespace
@@ -228,20 +238,16 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                                   float *d_time, hipStream_t s) {
   const char *ws = (const char *)a.ws;
   const Problem &p = a.p;
-  if (d_pos) {
-    const int64_t n = (int64_t)p.H * (2 * (int64_t)p.N - 1);
-    hipLaunchKernelGGL(finalize_pos_kernel, dim3((unsigned)((n + FIN_THREADS - 1) / FIN_THREADS)),
-                       dim3(FIN_THREADS), 0, s, (const SeqInfo *)(ws + a.L.seqinfo), p.B,
-                       (const float *)(ws + a.L.dpos_part), p.H, p.N, d_pos);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (d_time) {
-    const int width = p.H * p.nb;
-    hipLaunchKernelGGL(finalize_time_kernel, dim3((width + FIN_THREADS - 1) / FIN_THREADS),
-                       dim3(FIN_THREADS), 0, s, (const float *)(ws + a.L.dtime_part),
-                       a.L.dkv_grid, width, d_time);
-  }
+  const int pos_blocks = d_pos ? p.H * ((p.N + 63) / 64) : 0;
+  const int width = d_time ? p.H * p.nb : 0;
+  const int time_blocks = (width + 63) / 64;
+  if (pos_blocks + time_blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(finalize_tables_kernel, dim3(pos_blocks + time_blocks),
+                     dim3(FIN_THREADS), 0, s, (const SeqInfo *)(ws + a.L.seqinfo), p.B,
+                     d_pos ? (const float *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
+                     d_pos, pos_blocks,
+                     d_time ? (const float *)(ws + a.L.dtime_part) : nullptr,
+                     a.L.dkv_grid, width, d_time);
   return hipGetLastError();
 }
 

@@ -28,7 +28,7 @@ def run_gpu(w, bwd=True):
     out = dict(o=f.o, y=f.y, mean=f.ln_mean, rstd=f.ln_rstd)
     if bwd:
         g = plan.backward(q, k, v, u, off, to_dev(w.dy))
-        out.update(dq=g.dq, dk=g.dk, dv=g.dv, du=g.du, d_pos=g.d_pos, d_time=g.d_time)
+        out.update(dq=g.dq, dk=g.dk, dv=g.dv, du=g.du, d_pos=g.d_pos_w, d_time=g.d_time_w)
     torch.cuda.synchronize()
     return {n: (None if t is None else t.detach().to("cpu", torch.float64).numpy())
             for n, t in out.items()}
