@@ -185,7 +185,7 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   L.dkv_grid = bf16_bwd ? attn_dkv_grid(p, dev) : 0;
   L.dpos_part = (bf16_bwd && p.has_pos) ? take(sizeof(float) * (size_t)p.T * p.H) : 0;
   L.dtime_part = (bf16_bwd && p.has_time)
-                     ? take(sizeof(float) * (size_t)L.dkv_grid * p.H * p.nb)
+                     ? take(sizeof(float) * (size_t)DTIME_BINS * p.H * p.nb)
                      : 0;
   L.total = at;
   return L;

@@ -10,7 +10,7 @@
 //   attn_dkv   k-stationary: dV_j = sum_{i>=j} a_ij dO_i,
 //                            dK_j = sum_{i>=j} dS_ij q_i, plus the table
 //                            gradients (per-sequence diagonal partials for
-//                            d_pos, per-work-group histograms for d_time)
+//                            d_pos, binned per-work-group histograms for d_time)
 //
 // with s_ij = <q_i,k_j> + pos_w[h, j-i+N-1] + time_w[h, bucket(ts_i-ts_j)],
 // dS_ij = <dO_i, v_j> silu'(s_ij) / N, and the causal mask applied after the
@@ -26,8 +26,15 @@
 // Score accumulators come out with one fixed stationary row per lane, which
 // is exactly the operand layout of the accumulating product, so scores
 // never leave registers.  The two halves of the streamed side are summed
-// through LDS once per item.  The next streamed tile is fetched into
-// registers while the current one is being computed.
+// through LDS once per item.  The next streamed tile (with its bias slice and
+// timestamps) is fetched into registers while the current one computes.
+//
+// Relative-time bias fast path: while every timestamp of the tile pair lies
+// within 2^23 of the sequence's first one, |ts_i - ts_j| < 2^24 converts to
+// float exactly, and bits 21..30 of that float are 4*(e+127) + m with e =
+// floor(log2|x|) and m the two bits under the leading one -- the bucket
+// rule's own quantities.  A 604-entry LDS table per head maps that index
+// straight to the bias.  Otherwise the exact 64-bit rule is used.
 #include <algorithm>
 
 #include "internal.h"
@@ -40,6 +47,8 @@ namespace {
 constexpr int THREADS = 256;     // 4 waves
 constexpr int RM_PAD = 8;        // row-major LDS stride D+8 bf16
 constexpr int POS_COPY = 2 * TILE + 4;
+constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
+constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -70,36 +79,41 @@ struct TileRegs {
 
   __device__ __forceinline__ void load(const u16 *__restrict__ tile_base,
                                        int valid, int row_stride, int tid) {
+    if (valid >= TILE) {
 #pragma unroll
-    for (int x = 0; x < CPT; ++x) {
-      const int ch = tid + THREADS * x;
-      const int r = ch / (D / 8), d0 = (ch % (D / 8)) * 8;
-      c[x] = r < valid ? *(const uint4 *)(tile_base + r * row_stride + d0)
-                       : make_uint4(0, 0, 0, 0);
+      for (int x = 0; x < CPT; ++x) {
+        const int ch = tid + THREADS * x;
+        c[x] = *(const uint4 *)(tile_base + (ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8);
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < CPT; ++x) {
+        const int ch = tid + THREADS * x;
+        const int r = ch / (D / 8);
+        c[x] = r < valid ? *(const uint4 *)(tile_base + r * row_stride + (ch % (D / 8)) * 8)
+                         : make_uint4(0, 0, 0, 0);
+      }
     }
   }
   __device__ __forceinline__ void store(u16 *lds, int tid) const {
 #pragma unroll
     for (int x = 0; x < CPT; ++x) {
       const int ch = tid + THREADS * x;
-      const int r = ch / (D / 8), d0 = (ch % (D / 8)) * 8;
-      *(uint4 *)(lds + r * (D + RM_PAD) + d0) = c[x];
+      *(uint4 *)(lds + (ch / (D / 8)) * (D + RM_PAD) + (ch % (D / 8)) * 8) = c[x];
     }
   }
 };
 
-// A operand (or B operand of a score product) from a row-major LDS tile:
-// 8 consecutive d of row `row`, starting at column col.
+// 8 consecutive bf16 of row `row` of a row-major LDS tile, from column col.
 __device__ __forceinline__ bf16x8 read_rm(const u16 *lds, int stride, int row, int col) {
   return *(const bf16x8 *)(lds + row * stride + col);
 }
 
-// Operand holding, for lane l, column ncol + (l & 31) of rows
-// krow .. krow+3 and krow+8 .. krow+11 of a row-major LDS tile (krow
-// already includes this lane's 4*(l/32)), via two LDS transpose loads.
-// Within a 16-lane group, lane c addresses row (c>>2), columns 4*(c&3)..+3
-// of its group's 16-column slab; the transpose hands lane i the column
-// slab+i of the four rows.
+// Operand holding, for lane l, column ncol + (l & 31) of rows krow .. krow+3
+// and krow+8 .. krow+11 of a row-major LDS tile (krow already includes this
+// lane's 4*(l/32)), via two LDS transpose loads.  Within a 16-lane group,
+// lane c addresses row (c>>2), columns 4*(c&3)..+3 of its group's 16-column
+// slab; the transpose hands lane i the column slab+i of the four rows.
 __device__ __forceinline__ bf16x8 read_tr(const u16 *lds, int stride, int krow,
                                           int ncol, int lane) {
   const int c = lane & 15;
@@ -124,109 +138,49 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
     reg[ks] = as_bf16x8(ok ? *(const uint4 *)(p + 16 * ks) : make_uint4(0, 0, 0, 0));
 }
 
-// Position-bias slice of tile pair (qt, kt), stored four times with shifts
-// 0..3 so that any lane can read 4 consecutive entries with one aligned
-// 16-byte load: copy s, entry x = bias of local offset j_loc - i_loc =
-// x + s - 63.  Indices outside the table are only reached by masked pairs
-// and read as 0.
-__device__ __forceinline__ void stage_pos(const KParams &P, int h, int qt, int kt,
-                                          float *pos, int tid) {
-  const int64_t span = 2 * (int64_t)P.N - 1;
-  const int64_t base = (int64_t)(kt - qt) * TILE + P.N - 1 - (TILE - 1);
-  const float *tab = P.pos_w + (int64_t)h * span;
-  for (int x = tid; x < 4 * POS_COPY; x += THREADS) {
-    const int s = x / POS_COPY, e = x % POS_COPY;
-    const int64_t idx = base + e + s;
-    pos[x] = (idx >= 0 && idx < span) ? tab[idx] : 0.0f;
+// Position-bias slice of tile pair (qt, kt): entry x (0..126) is the bias of
+// local offset j_loc - i_loc = x - 63, i.e. pos_w[h, (kt-qt)*64 + x - 63 +
+// N - 1]; indices outside the table are only reached by masked pairs and
+// read as 0.  Thread x fetches entry x one tile ahead (pos_fetch); the store
+// writes it into four LDS copies shifted by 0..3 so that 4 consecutive
+// entries are one aligned 16-byte load for any lane: forward order (copy s,
+// entry x - s) for the q-stationary kernels, reversed order (copy s, entry
+// 126 - x - s) for the k-stationary one, whose lanes walk the offsets
+// downwards.  Threads with nothing to store write a never-read pad slot.
+__device__ __forceinline__ float pos_fetch(const KParams &P, int h, int qt, int kt, int tid) {
+  const int span = 2 * P.N - 1;
+  const int idx = (kt - qt) * TILE + P.N - TILE + tid;
+  return (tid < 2 * TILE - 1 && idx >= 0 && idx < span) ? P.pos_w[(int64_t)h * span + idx] : 0.0f;
+}
+
+template <bool REVERSED>
+__device__ __forceinline__ void pos_store(float v, float *pos, int tid) {
+  const int x = REVERSED ? 2 * TILE - 2 - tid : tid;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const bool ok = tid < 2 * TILE - 1 && x >= s;
+    pos[s * POS_COPY + (ok ? x - s : POS_COPY - 1)] = v;
   }
 }
 
-// Bias lookups of one lane: 16 consecutive-in-register scores whose
-// streamed-side local index is sbase + c_row(r, g) and whose stationary
-// local index is `st`.  Returns a pointer p such that p[c_row(r,g)-4g]
-// is the position bias of register r; aligned for 16-byte reads.
-//   q-stationary (fwd, dq): offset = j - i = (sbase + 4g + c) - st
-//   k-stationary (dkv):     offset = j - i = st - (sbase + 4g + c)
-// handled by the callers through the sign of the register walk.
-__device__ __forceinline__ const float *pos_lane_q(const float *pos, int st, int sbase, int g) {
-  const int x0 = sbase + 4 * g - st + (TILE - 1);     // x for c_row offset 0, >= 0
+// Aligned pointer to 4 consecutive slice entries starting at entry x0 (any
+// x0 >= 0): copy x0 & 3, entry x0 - (x0 & 3).
+__device__ __forceinline__ const float *pos_lane(const float *pos, int x0) {
   const int s = x0 & 3;
   return pos + s * POS_COPY + (x0 - s);
 }
 
-// 32-bit time bucket of |d| (exact for |d| < 2^31): branch-free.
-__device__ __forceinline__ int bucket32(int32_t dlt, int nb) {
-  const uint32_t x = (uint32_t)(dlt < 0 ? -dlt : dlt);
-  const int e = 31 - __builtin_clz(x | 1u);
-  const uint32_t m = __builtin_amdgcn_ubfe(x, (uint32_t)(e - 2) & 31u, 2u);
-  int b = 4 * e - 4 + (int)m;
-  b = x < 4u ? (int)x : b;
+// Float-exponent index of an exact |delta| < 2^24 (see file comment).
+__device__ __forceinline__ int time_index(int32_t delta) {
+  return (int)__builtin_amdgcn_ubfe(__float_as_uint((float)delta), 21u, 10u);
+}
+
+// Bucket of float-exponent index k (k = 0 <-> 0; 508, 512, 514 <-> 1, 2, 3;
+// k >= 516 <-> k - 512), clamped to nb-1.  Indices no integer reaches map
+// to some valid bucket.
+__device__ __forceinline__ int bucket_of_index(int k, int nb) {
+  int b = k >= 516 ? k - 512 : (k >= 514 ? 3 : (k >= 512 ? 2 : (k >= 508 ? 1 : 0)));
   return b < nb - 1 ? b : nb - 1;
-}
-
-// Relative-time bucket of a pair: the 32-bit path on timestamps relative to
-// the sequence start (exact while both lie within +-2^30 of it), else the
-// 64-bit rule on the raw timestamps.
-template <bool SLOW>
-__device__ __forceinline__ int pair_bucket(int32_t a32, int32_t b32, int64_t a64,
-                                           int64_t b64, int nb) {
-  return SLOW ? time_bucket(a64 - b64, nb) : bucket32(a32 - b32, nb);
-}
-
-// Biased scores of a q-stationary lane (query i fixed, 16 keys): x[r] =
-// s[r] + pos bias + time bias.  pl: this lane's aligned position-bias
-// pointer; tk / tk64: key timestamps of its first key (32-bit relative /
-// raw); the lane's keys sit at offsets 8*q4 + c, c = 0..3.
-template <bool POS, bool TIME, bool SLOW>
-__device__ __forceinline__ void biased_scores_q(const f32x16 &s, float (&x)[16],
-                                                const float *pl, const int32_t *tk,
-                                                const int64_t *tk64, const float *tw,
-                                                int32_t ts_i32, int64_t ts_i, int nb) {
-#pragma unroll
-  for (int q4 = 0; q4 < 4; ++q4) {
-    const float4 pb = POS ? *(const float4 *)(pl + 8 * q4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    const int4 t4 = (TIME && !SLOW) ? *(const int4 *)(tk + 8 * q4) : make_int4(0, 0, 0, 0);
-    const float pbv[4] = {pb.x, pb.y, pb.z, pb.w};
-    const int32_t tv[4] = {t4.x, t4.y, t4.z, t4.w};
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      float v = s[4 * q4 + c];
-      if (POS) v += pbv[c];
-      if (TIME) {
-        const int64_t t64 = SLOW ? tk64[8 * q4 + c] : 0;
-        v += tw[pair_bucket<SLOW>(ts_i32, tv[c], ts_i, t64, nb)];
-      }
-      x[4 * q4 + c] = v;
-    }
-  }
-}
-
-// Biased scores of a k-stationary lane (key j fixed, 16 queries at offsets
-// i_rel = 8*q4 + c from its first query): position bias at pos[x0 - i_rel]
-// (descending), time bias of ts_i - ts_j; bk[r] receives the bucket.
-template <bool POS, bool TIME, bool SLOW>
-__device__ __forceinline__ void biased_scores_k(const f32x16 &s, float (&x)[16], int (&bk)[16],
-                                                const float *pos, int x0, const int32_t *tq,
-                                                const int64_t *tq64, const float *tw,
-                                                int32_t ts_j32, int64_t ts_j, int nb) {
-#pragma unroll
-  for (int q4 = 0; q4 < 4; ++q4) {
-    const int4 t4 = (TIME && !SLOW) ? *(const int4 *)(tq + 8 * q4) : make_int4(0, 0, 0, 0);
-    const int32_t tv[4] = {t4.x, t4.y, t4.z, t4.w};
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int r = 4 * q4 + c, i_rel = 8 * q4 + c;
-      float v = s[r];
-      if (POS) v += pos[x0 - i_rel];
-      bk[r] = 0;
-      if (TIME) {
-        const int64_t t64 = SLOW ? tq64[i_rel] : 0;
-        bk[r] = pair_bucket<SLOW>(tv[c], ts_j32, t64, ts_j, nb);
-        v += tw[bk[r]];
-      }
-      x[r] = v;
-    }
-  }
 }
 
 // silu(x) / N = x / (N (1 + e^-x)); hardware exp2 and reciprocal.
@@ -235,7 +189,11 @@ __device__ __forceinline__ float silu_over_n(float x, float n) {
   return x * __builtin_amdgcn_rcpf(__builtin_fmaf(n, t, n));
 }
 
-constexpr int32_t REL_LIMIT = 1 << 30;   // |ts - ts_start| below this -> 32-bit deltas
+// silu'(x) / N = sigma(x) (1 + x (1 - sigma(x))) / N
+__device__ __forceinline__ float dsilu_over_n(float x, float inv_n) {
+  const float sg = sigmoid_f(x);
+  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * inv_n;
+}
 
 template <int D>
 struct StreamSmem {
@@ -247,33 +205,71 @@ struct StreamSmem {
     float red[2][32 * D];                // cross-wave sums at the end of an item
   };
   alignas(16) float pos[4 * POS_COPY];
-  alignas(16) int32_t ts32[TILE];
-  int64_t ts64[TILE];
+  alignas(16) int32_t ts32[TILE];        // streamed-tile timestamps - ts_start
+  int64_t ts64[TILE];                    // raw streamed-tile timestamps
+  float ktab[KTAB];                      // float-exponent index -> time bias
+  int flag[2];                           // "some timestamp is far" (parity-buffered)
   int item;
 };
 
-__device__ __forceinline__ int pop_item(const KParams &P, int &slot_item, int tid) {
-  if (tid == 0) slot_item = atomicAdd(P.pop, 1);
-  __syncthreads();
-  return slot_item;
+// Per-lane running sum of d_time contributions over one time index (the
+// lane's pairs visit non-decreasing indices when timestamps are ordered, so
+// a run is flushed only when its index changes).
+struct TimeRun {
+  float sum = 0.0f;
+  int cur = -1;
+  __device__ __forceinline__ void add(float *acc, int k, float v) {
+    if (k != cur) {
+      if (cur >= 0) atomicAdd(&acc[cur], sum);
+      cur = k;
+      sum = 0.0f;
+    }
+    sum += v;
+  }
+  __device__ __forceinline__ void flush(float *acc) {
+    if (cur >= 0) atomicAdd(&acc[cur], sum);
+    cur = -1;
+    sum = 0.0f;
+  }
+};
+
+// Item-level set-up shared by the kernels: time tables of head h.
+template <int D>
+__device__ __forceinline__ void stage_time_tables(const KParams &P, StreamSmem<D> &sm,
+                                                  float *tw, int h, int tid) {
+  const float *tab = P.time_w + (int64_t)h * P.nb;
+  for (int x = tid; x < P.nb; x += THREADS) tw[x] = tab[x];
+  for (int x = tid; x < KTAB; x += THREADS) sm.ktab[x] = tab[bucket_of_index(x, P.nb)];
 }
 
 // ---------------------------------------------------------------- forward
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS)
+__global__ void __launch_bounds__(THREADS, 2)
 attn_fwd_kernel(KParams P) {
   __shared__ StreamSmem<D> sm;
   extern __shared__ float tw[];               // time_w row of the item's head
   constexpr int ST = D + RM_PAD;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int g = lane >> 5, l32 = lane & 31;
-  const int wi = w & 1, wj = w >> 1;          // query half, key half
+  const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  const int row_stride = P.H * D;
+  if (tid0 < 2) sm.flag[tid0] = 0;
+  int phase = 0;
 
   for (;;) {
-    const int item = pop_item(P, sm.item, tid);
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
+    lds_barrier();
+    const int item = sm.item;
     if (item >= n_items) break;
+    // Lane-derived values are rebuilt per item from an opaque copy of the
+    // thread index: otherwise the compiler hoists dozens of per-lane
+    // addresses out of the persistent loop and pins their registers.
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    int row_stride = P.H * D;
+    asm volatile("" : "+s"(row_stride));
+    const int lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wi = w & 1, wj = w >> 1;        // query half, key half
+
     const WorkEntry e = P.list[item / P.H];
     const int h = item % P.H;
     const SeqInfo si = P.info[e.seq];
@@ -287,14 +283,14 @@ attn_fwd_kernel(KParams P) {
 
     int64_t ts_start = 0, ts_i = 0;
     int32_t ts_i32 = 0;
-    bool item_slow = false;
+    bool q_far = false;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
-      for (int x = tid; x < P.nb; x += THREADS) tw[x] = P.time_w[(int64_t)h * P.nb + x];
-      item_slow = __syncthreads_or(rel >= REL_LIMIT || rel <= -REL_LIMIT);
+      q_far = rel >= NEAR || rel <= -NEAR;
+      stage_time_tables<D>(P, sm, tw, h, tid);
     }
 
     f32x16 oacc[D / 32];
@@ -305,38 +301,39 @@ attn_fwd_kernel(KParams P) {
 
     TileRegs<D> kr, vr;
     int64_t ts_k = 0;
+    float pos_v = 0.0f;
     {
-      const u16 *kb = P.k + ((si.start) * P.H + h) * (int64_t)D;
-      const u16 *vb = P.v + ((si.start) * P.H + h) * (int64_t)D;
-      kr.load(kb, si.len, row_stride, tid);
-      vr.load(vb, si.len, row_stride, tid);
+      kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
+      vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
       if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
+      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
     }
 
-    for (int kt = 0; kt <= qt; ++kt) {
-      __syncthreads();
+    for (int kt = 0; kt <= qt; ++kt, ++phase) {
+      lds_barrier();
       kr.store(sm.t.a, tid);
       vr.store(sm.t.b, tid);
-      if (POS) stage_pos(P, h, qt, kt, sm.pos, tid);
-      bool tile_slow = item_slow;
+      if (POS) pos_store<false>(pos_v, sm.pos, tid);
       if (TIME) {
-        int far = 0;
+        bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
           sm.ts32[tid] = (int32_t)rel;
           sm.ts64[tid] = ts_k;
-          far = rel >= REL_LIMIT || rel <= -REL_LIMIT;
+          far |= rel >= NEAR || rel <= -NEAR;
         }
-        tile_slow |= __syncthreads_or(far) != 0;
-      } else {
-        __syncthreads();
+        if (far) sm.flag[phase & 1] = 1;
       }
+      lds_barrier();
+      const bool slow = TIME && sm.flag[phase & 1] != 0;
+      if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
       if (kt < qt) {       // prefetch the next key tile while this one computes
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       }
 
       // S^T quadrant [32 keys x 32 queries] = K_wj Q_wi^T
@@ -347,23 +344,44 @@ attn_fwd_kernel(KParams P) {
       for (int ks = 0; ks < D / 16; ++ks)
         s = mfma32(read_rm(sm.t.a, ST, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
 
-      // a_ij = silu(s_ij + bias) / N; causal mask (after the SiLU) only on
-      // the diagonal tile
-      const float *pl = POS ? pos_lane_q(sm.pos, i_loc, 32 * wj, g) : nullptr;
-      const int32_t *tk = sm.ts32 + 32 * wj + 4 * g;
-      const int64_t *tk64 = sm.ts64 + 32 * wj + 4 * g;
+      // bias: this lane's keys sit at 32 wj + 4 g + 8 q4 + c
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = s[r];
+      const int kb = 32 * wj + 4 * g;
+      if (POS) {
+        const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pb = *(const float4 *)(pl + 8 * q4);
+          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
+          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+        }
+      }
+      if (TIME) {
+        if (!slow) {
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
+            x[4 * q4 + 0] += sm.ktab[time_index(ts_i32 - t4.x)];
+            x[4 * q4 + 1] += sm.ktab[time_index(ts_i32 - t4.y)];
+            x[4 * q4 + 2] += sm.ktab[time_index(ts_i32 - t4.z)];
+            x[4 * q4 + 3] += sm.ktab[time_index(ts_i32 - t4.w)];
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            x[r] += tw[time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
+        }
+      }
       const float fN = (float)P.N;
       float av[16];
-      if (TIME && tile_slow)
-        biased_scores_q<POS, TIME, true>(s, av, pl, tk, tk64, tw, ts_i32, ts_i, P.nb);
-      else
-        biased_scores_q<POS, TIME, false>(s, av, pl, tk, tk64, tw, ts_i32, ts_i, P.nb);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) av[r] = silu_over_n(av[r], fN);
+      for (int r = 0; r < 16; ++r) av[r] = silu_over_n(x[r], fN);
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (32 * wj + c_row(r, g) > i_loc) av[r] = 0.0f;
+          if (kb + c_row(r, 0) > i_loc) av[r] = 0.0f;
       }
 
       // O_wi += P V over this wave's 32 keys (two 16-key k-steps)
@@ -383,15 +401,15 @@ attn_fwd_kernel(KParams P) {
     }
 
     // sum the two key halves, store O (bf16)
-    __syncthreads();
+    lds_barrier();
     if (wj == 1) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          sm.red[wi][(c_row(r, g)) * D + 32 * db + l32] = oacc[db][r];
+          sm.red[wi][c_row(r, g) * D + 32 * db + l32] = oacc[db][r];
     }
-    __syncthreads();
+    lds_barrier();
     if (wj == 0) {
       u16 *o = P.out0 + ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
 #pragma unroll
@@ -411,20 +429,29 @@ attn_fwd_kernel(KParams P) {
 
 // --------------------------------------------------------------------- dQ
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS)
+__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_dq_kernel(KParams P) {
   __shared__ StreamSmem<D> sm;
   extern __shared__ float tw[];
   constexpr int ST = D + RM_PAD;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int g = lane >> 5, l32 = lane & 31;
-  const int wi = w & 1, wj = w >> 1;
+  const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  const int row_stride = P.H * D;
+  if (tid0 < 2) sm.flag[tid0] = 0;
+  int phase = 0;
 
   for (;;) {
-    const int item = pop_item(P, sm.item, tid);
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
+    lds_barrier();
+    const int item = sm.item;
     if (item >= n_items) break;
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    int row_stride = P.H * D;
+    asm volatile("" : "+s"(row_stride));
+    const int lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wi = w & 1, wj = w >> 1;
+
     const WorkEntry e = P.list[item / P.H];
     const int h = item % P.H;
     const SeqInfo si = P.info[e.seq];
@@ -439,14 +466,14 @@ attn_dq_kernel(KParams P) {
 
     int64_t ts_start = 0, ts_i = 0;
     int32_t ts_i32 = 0;
-    bool item_slow = false;
+    bool q_far = false;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
-      for (int x = tid; x < P.nb; x += THREADS) tw[x] = P.time_w[(int64_t)h * P.nb + x];
-      item_slow = __syncthreads_or(rel >= REL_LIMIT || rel <= -REL_LIMIT);
+      q_far = rel >= NEAR || rel <= -NEAR;
+      stage_time_tables<D>(P, sm, tw, h, tid);
     }
 
     f32x16 acc[D / 32];
@@ -457,37 +484,39 @@ attn_dq_kernel(KParams P) {
 
     TileRegs<D> kr, vr;
     int64_t ts_k = 0;
+    float pos_v = 0.0f;
     {
-      const int64_t r0 = si.start;
-      kr.load(P.k + (r0 * P.H + h) * D, si.len, row_stride, tid);
-      vr.load(P.v + (r0 * P.H + h) * D, si.len, row_stride, tid);
-      if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[r0 + tid] : ts_start;
+      kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
+      vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
+      if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
+      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
     }
 
-    for (int kt = 0; kt <= qt; ++kt) {
-      __syncthreads();
+    for (int kt = 0; kt <= qt; ++kt, ++phase) {
+      lds_barrier();
       kr.store(sm.t.a, tid);
       vr.store(sm.t.b, tid);
-      if (POS) stage_pos(P, h, qt, kt, sm.pos, tid);
-      bool tile_slow = item_slow;
+      if (POS) pos_store<false>(pos_v, sm.pos, tid);
       if (TIME) {
-        int far = 0;
+        bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
           sm.ts32[tid] = (int32_t)rel;
           sm.ts64[tid] = ts_k;
-          far = rel >= REL_LIMIT || rel <= -REL_LIMIT;
+          far |= rel >= NEAR || rel <= -NEAR;
         }
-        tile_slow |= __syncthreads_or(far) != 0;
-      } else {
-        __syncthreads();
+        if (far) sm.flag[phase & 1] = 1;
       }
+      lds_barrier();
+      const bool slow = TIME && sm.flag[phase & 1] != 0;
+      if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
       if (kt < qt) {
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       }
 
       f32x16 s, da;
@@ -499,24 +528,42 @@ attn_dq_kernel(KParams P) {
         da = mfma32(read_rm(sm.t.b, ST, 32 * wj + l32, 16 * ks + 8 * g), doreg[ks], da);
       }
 
-      const float *pl = POS ? pos_lane_q(sm.pos, i_loc, 32 * wj, g) : nullptr;
-      const int32_t *tk = sm.ts32 + 32 * wj + 4 * g;
-      const int64_t *tk64 = sm.ts64 + 32 * wj + 4 * g;
-      float dsv[16];
-      if (TIME && tile_slow)
-        biased_scores_q<POS, TIME, true>(s, dsv, pl, tk, tk64, tw, ts_i32, ts_i, P.nb);
-      else
-        biased_scores_q<POS, TIME, false>(s, dsv, pl, tk, tk64, tw, ts_i32, ts_i, P.nb);
+      float x[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float x = dsv[r];
-        const float sg = sigmoid_f(x);
-        dsv[r] = da[r] * sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * P.inv_n;
+      for (int r = 0; r < 16; ++r) x[r] = s[r];
+      const int kb = 32 * wj + 4 * g;
+      if (POS) {
+        const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pb = *(const float4 *)(pl + 8 * q4);
+          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
+          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+        }
       }
+      if (TIME) {
+        if (!slow) {
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
+            x[4 * q4 + 0] += sm.ktab[time_index(ts_i32 - t4.x)];
+            x[4 * q4 + 1] += sm.ktab[time_index(ts_i32 - t4.y)];
+            x[4 * q4 + 2] += sm.ktab[time_index(ts_i32 - t4.z)];
+            x[4 * q4 + 3] += sm.ktab[time_index(ts_i32 - t4.w)];
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            x[r] += tw[time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
+        }
+      }
+      float dsv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu_over_n(x[r], P.inv_n);
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (32 * wj + c_row(r, g) > i_loc) dsv[r] = 0.0f;
+          if (kb + c_row(r, 0) > i_loc) dsv[r] = 0.0f;
       }
 
 #pragma unroll
@@ -534,7 +581,7 @@ attn_dq_kernel(KParams P) {
       }
     }
 
-    __syncthreads();
+    lds_barrier();
     if (wj == 1) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
@@ -542,7 +589,7 @@ attn_dq_kernel(KParams P) {
         for (int r = 0; r < 16; ++r)
           sm.red[wi][c_row(r, g) * D + 32 * db + l32] = acc[db][r];
     }
-    __syncthreads();
+    lds_barrier();
     if (wj == 0) {
       u16 *dq = P.out0 + qoff;
 #pragma unroll
@@ -561,34 +608,52 @@ attn_dq_kernel(KParams P) {
 }
 
 // ------------------------------------------------------------------ dK/dV
-template <int D>
+// d_pos of a tile pair without LDS atomics (which cost hundreds of cycles
+// per instruction here): every lane stores its dS values "sheared" -- row
+// i, column j - i + 63 -- so that each diagonal becomes one column, and the
+// columns are then summed with plain loads.  The odd row stride keeps both
+// the stores (fixed i, consecutive j) and the column reads bank-conflict free.
+constexpr int SHEAR_STRIDE = 2 * TILE + 9;
+
+template <int D, bool POS>
 struct DkvSmem {
   StreamSmem<D> s;
-  float diag_acc[2 * TILE];     // d_pos of the current tile pair by local offset
+  float shear[POS ? TILE * SHEAR_STRIDE : 1];
+  float kacc[KTAB];             // this item's d_time by float-exponent index
 };
 
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS)
+__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_dkv_kernel(KParams P) {
-  __shared__ DkvSmem<D> smx;
+  __shared__ DkvSmem<D, POS> smx;
   StreamSmem<D> &sm = smx.s;
   extern __shared__ float dyn[];             // [nb] time_w row, then [H][nb] d_time
   float *tw = dyn;
   float *tacc = dyn + P.nb;
   constexpr int ST = D + RM_PAD;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int g = lane >> 5, l32 = lane & 31;
-  const int wj = w & 1, wi = w >> 1;          // key half (stationary), query half
+  const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  const int row_stride = P.H * D;
 
-  if (TIME)
-    for (int x = tid; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0f;
-  for (int x = tid; x < 2 * TILE; x += THREADS) smx.diag_acc[x] = 0.0f;
+  if (TIME) {
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0f;
+    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0f;
+  }
+  if (tid0 < 2) sm.flag[tid0] = 0;
+  int phase = 0;
 
   for (;;) {
-    const int item = pop_item(P, sm.item, tid);
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
+    lds_barrier();
+    const int item = sm.item;
     if (item >= n_items) break;
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    int row_stride = P.H * D;
+    asm volatile("" : "+s"(row_stride));
+    const int lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wj = w & 1, wi = w >> 1;        // key half (stationary), query half
+
     const WorkEntry e = P.list[item / P.H];
     const int h = item % P.H;
     const SeqInfo si = P.info[e.seq];
@@ -603,21 +668,17 @@ attn_dkv_kernel(KParams P) {
 
     int64_t ts_start = 0, ts_j = 0;
     int32_t ts_j32 = 0;
-    bool item_slow = false;
+    bool k_far = false;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_j = j_loc < k_valid ? P.ts[si.start + (int64_t)kt * TILE + j_loc] : ts_start;
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (int32_t)rel;
-      for (int x = tid; x < P.nb; x += THREADS) tw[x] = P.time_w[(int64_t)h * P.nb + x];
-      item_slow = __syncthreads_or(rel >= REL_LIMIT || rel <= -REL_LIMIT);
+      k_far = rel >= NEAR || rel <= -NEAR;
+      stage_time_tables<D>(P, sm, tw, h, tid);
     }
+    TimeRun run;                              // fast path: by float-exponent index
     float *my_t = TIME ? tacc + h * P.nb : nullptr;
-    // run-length pre-combined d_time: this lane's pairs (its key against
-    // increasing queries) visit non-decreasing buckets when timestamps are
-    // ordered, so a run is flushed only when its bucket changes
-    float tsum = 0.0f;
-    int tcur = -1;
 
     f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -627,39 +688,40 @@ attn_dkv_kernel(KParams P) {
 
     TileRegs<D> qr, dr;
     int64_t ts_q = 0;
+    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid) : 0.0f;
     {
-      const int q_valid = si.len - kt * TILE;
       const int64_t r0 = si.start + (int64_t)kt * TILE;
-      qr.load(P.q + (r0 * P.H + h) * D, q_valid, row_stride, tid);
-      dr.load(P.dO + (r0 * P.H + h) * D, q_valid, row_stride, tid);
-      if (TIME && tid < TILE) ts_q = tid < q_valid ? P.ts[r0 + tid] : ts_start;
+      qr.load(P.q + (r0 * P.H + h) * D, k_valid, row_stride, tid);
+      dr.load(P.dO + (r0 * P.H + h) * D, k_valid, row_stride, tid);
+      if (TIME && tid < TILE) ts_q = tid < k_valid ? P.ts[r0 + tid] : ts_start;
     }
 
-    for (int qt = kt; qt < si.ntiles; ++qt) {
+    for (int qt = kt; qt < si.ntiles; ++qt, ++phase) {
       const int q_valid = si.len - qt * TILE;
-      __syncthreads();
+      lds_barrier();
       qr.store(sm.t.a, tid);
       dr.store(sm.t.b, tid);
-      if (POS) stage_pos(P, h, qt, kt, sm.pos, tid);
-      bool tile_slow = item_slow;
+      if (POS) pos_store<true>(pos_v, sm.pos, tid);
       if (TIME) {
-        int far = 0;
+        bool far = k_far;
         if (tid < TILE) {
           const int64_t rel = ts_q - ts_start;
           sm.ts32[tid] = (int32_t)rel;
           sm.ts64[tid] = ts_q;
-          far = rel >= REL_LIMIT || rel <= -REL_LIMIT;
+          far |= rel >= NEAR || rel <= -NEAR;
         }
-        tile_slow |= __syncthreads_or(far) != 0;
-      } else {
-        __syncthreads();
+        if (far) sm.flag[phase & 1] = 1;
       }
+      lds_barrier();
+      const bool slow = TIME && sm.flag[phase & 1] != 0;
+      if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
       if (qt + 1 < si.ntiles) {
         const int nv = si.len - (qt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
         qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
         dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
         if (TIME && tid < TILE) ts_q = tid < nv ? P.ts[r0 + tid] : ts_start;
+        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid);
       }
 
       // S and dA quadrants [32 queries x 32 keys]; lane holds key j_loc
@@ -672,37 +734,73 @@ attn_dkv_kernel(KParams P) {
         da = mfma32(read_rm(sm.t.b, ST, 32 * wi + l32, 16 * ks + 8 * g), vreg[ks], da);
       }
 
-      // offset j - i = j_loc - (32 wi + 4 g + c_row'): walk the position
-      // slice downwards from x0 = j_loc - 32 wi - 4 g + 63
-      const int x0 = j_loc - 32 * wi - 4 * g + (TILE - 1);
-      const int32_t *tq = sm.ts32 + 32 * wi + 4 * g;
-      const int64_t *tq64 = sm.ts64 + 32 * wi + 4 * g;
+      // this lane's queries sit at ib + 8 q4 + c, ib = 32 wi + 4 g; offset
+      // j - i = j_loc - ib - i_rel walks the slice downwards, i.e. the
+      // reversed copies upwards from 126 - x0
+      const int ib = 32 * wi + 4 * g;
+      const int x0 = j_loc - ib + (TILE - 1);
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = s[r];
+      if (POS) {
+        const float *pl = pos_lane(sm.pos, 2 * TILE - 2 - x0);
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pb = *(const float4 *)(pl + 8 * q4);
+          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
+          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+        }
+      }
+      int tk[16];
+      if (TIME) {
+        if (!slow) {
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * q4);
+            tk[4 * q4 + 0] = time_index(t4.x - ts_j32);
+            tk[4 * q4 + 1] = time_index(t4.y - ts_j32);
+            tk[4 * q4 + 2] = time_index(t4.z - ts_j32);
+            tk[4 * q4 + 3] = time_index(t4.w - ts_j32);
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r) x[r] += sm.ktab[tk[r]];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            tk[r] = time_bucket(sm.ts64[ib + c_row(r, 0)] - ts_j, P.nb);
+            x[r] += tw[tk[r]];
+          }
+        }
+      }
       const bool diag = (qt == kt);
       float av[16], dsv[16];
-      int bk[16];
-      if (TIME && tile_slow)
-        biased_scores_k<POS, TIME, true>(s, av, bk, sm.pos, x0, tq, tq64, tw, ts_j32, ts_j, P.nb);
-      else
-        biased_scores_k<POS, TIME, false>(s, av, bk, sm.pos, x0, tq, tq64, tw, ts_j32, ts_j, P.nb);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int i_rel = 8 * (r >> 2) + (r & 3);          // c_row(r, g) - 4g
-        const int i_loc = 32 * wi + 4 * g + i_rel;
+        const int i_loc = ib + c_row(r, 0);
         const bool valid = (i_loc < q_valid) && (!diag || i_loc >= j_loc);
-        const float x = av[r];
-        const float sg = sigmoid_f(x);
-        const float a = x * sg * P.inv_n;
-        const float ds = da[r] * sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * P.inv_n;
+        const float sg = sigmoid_f(x[r]);
+        const float a = x[r] * sg * P.inv_n;
+        const float ds = da[r] * sg * __builtin_fmaf(x[r], 1.0f - sg, 1.0f) * P.inv_n;
         av[r] = valid ? a : 0.0f;
         dsv[r] = valid ? ds : 0.0f;
-        if (POS && valid) atomicAdd(&smx.diag_acc[x0 - i_rel], ds);
-        if (TIME && valid) {
-          if (bk[r] != tcur) {
-            if (tcur >= 0) atomicAdd(&my_t[tcur], tsum);
-            tcur = bk[r];
-            tsum = 0.0f;
-          }
-          tsum += ds;
+      }
+      if (POS) {
+        // element (i, j) -> shear[i][j - i + 63]; i = ib + c_row(r, 0)
+        float *sh = smx.shear + ib * SHEAR_STRIDE + x0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sh[c_row(r, 0) * (SHEAR_STRIDE - 1)] = dsv[r];
+      }
+      if (TIME) {
+        // slow tiles accumulate by bucket straight into the work-group
+        // histogram; fast tiles by float-exponent index, folded per item
+        if (!slow) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (dsv[r] != 0.0f) run.add(smx.kacc, tk[r], dsv[r]);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (dsv[r] != 0.0f) atomicAdd(&my_t[tk[r]], dsv[r]);
         }
       }
 
@@ -727,22 +825,36 @@ attn_dkv_kernel(KParams P) {
         }
       }
       if (POS) {
-        // the diagonals of this tile pair are complete: fold them into the
-        // sequence's d_pos partial (index m = i - j >= 0)
-        __syncthreads();
-        if (tid < 2 * TILE - 1) {
-          const float val = smx.diag_acc[tid];
-          smx.diag_acc[tid] = 0.0f;
-          const int m = (qt - kt) * TILE - (tid - (TILE - 1));
+        // the diagonals of this tile pair are complete: sum column c (local
+        // offset j - i = c - 63) over one half of its rows and fold it into
+        // the sequence's d_pos partial (index m = i - j >= 0)
+        lds_barrier();
+        const int c = tid & 127, half = tid >> 7;
+        if (c < 2 * TILE - 1) {
+          const int lo = max(32 * half, TILE - 1 - c);
+          const int hi = min(32 * half + 32, 2 * TILE - 1 - c);
+          float val = 0.0f;
+          for (int i = lo; i < hi; ++i) val += smx.shear[i * SHEAR_STRIDE + c];
+          const int m = (qt - kt) * TILE - (c - (TILE - 1));
           if (val != 0.0f && m >= 0 && m < si.len)
             atomicAdd(&P.dpos_part[(si.start + m) * P.H + h], val);
         }
       }
     }
-    if (TIME && tcur >= 0) atomicAdd(&my_t[tcur], tsum);
 
-    // sum the two query halves, store dK, dV (bf16)
-    __syncthreads();
+    // sum the two query halves, store dK, dV (bf16); fold this item's
+    // d_time by index into the work-group histogram
+    if (TIME) run.flush(smx.kacc);
+    lds_barrier();
+    if (TIME) {
+      for (int x = tid; x < KTAB; x += THREADS) {
+        const float val = smx.kacc[x];
+        if (val != 0.0f) {
+          smx.kacc[x] = 0.0f;
+          atomicAdd(&my_t[bucket_of_index(x, P.nb)], val);
+        }
+      }
+    }
     if (wi == 1) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
@@ -750,14 +862,14 @@ attn_dkv_kernel(KParams P) {
         for (int r = 0; r < 16; ++r)
           sm.red[wj][c_row(r, g) * D + 32 * db + l32] = dk[db][r];
     }
-    __syncthreads();
+    lds_barrier();
     if (wi == 0) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) dk[db][r] += sm.red[wj][c_row(r, g) * D + 32 * db + l32];
     }
-    __syncthreads();
+    lds_barrier();
     if (wi == 1) {
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
@@ -765,7 +877,7 @@ attn_dkv_kernel(KParams P) {
         for (int r = 0; r < 16; ++r)
           sm.red[wj][c_row(r, g) * D + 32 * db + l32] = dv[db][r];
     }
-    __syncthreads();
+    lds_barrier();
     if (wi == 0) {
       u16 *dko = P.out0 + koff;
       u16 *dvo = P.out1 + koff;
@@ -784,9 +896,11 @@ attn_dkv_kernel(KParams P) {
     }
   }
   if (TIME) {
-    __syncthreads();
-    float *part = P.dtime_part + (int64_t)blockIdx.x * P.H * P.nb;
-    for (int x = tid; x < P.H * P.nb; x += THREADS) part[x] = tacc[x];
+    // fold this work-group's histogram into one of DTIME_BINS partials
+    lds_barrier();
+    float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
+    for (int x = tid0; x < P.H * P.nb; x += THREADS)
+      if (tacc[x] != 0.0f) atomicAdd(&part[x], tacc[x]);
   }
 }
 
@@ -842,29 +956,31 @@ int current_dev() {
   return dev;
 }
 
+size_t q_dyn_bytes(const Problem &p) { return p.has_time ? sizeof(float) * p.nb : 0; }
+size_t k_dyn_bytes(const Problem &p) {
+  return p.has_time ? sizeof(float) * (size_t)p.nb * (p.H + 1) : 0;
+}
+
 }  // namespace
 
 int attn_fwd_grid(const Problem &p, int dev) {
   int grid = 1;
-  const size_t dyn = p.has_time ? sizeof(float) * p.nb : 0;
   HSTU_DISPATCH(attn_fwd_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, dyn, p.max_entries * p.H, dev));
+                grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
   return grid;
 }
 
 int attn_dq_grid(const Problem &p, int dev) {
   int grid = 1;
-  const size_t dyn = p.has_time ? sizeof(float) * p.nb : 0;
   HSTU_DISPATCH(attn_dq_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, dyn, p.max_entries * p.H, dev));
+                grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
   return grid;
 }
 
 int attn_dkv_grid(const Problem &p, int dev) {
   int grid = 1;
-  const size_t dyn = p.has_time ? sizeof(float) * (size_t)p.nb * (p.H + 1) : 0;
   HSTU_DISPATCH(attn_dkv_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, dyn, p.max_entries * p.H, dev));
+                grid = persistent_grid(kfn, k_dyn_bytes(p), p.max_entries * p.H, dev));
   return grid;
 }
 
@@ -875,9 +991,8 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
   P.out0 = (u16 *)o;
   const Problem &p = a.p;
   const int grid = attn_fwd_grid(p, current_dev());
-  const size_t dyn = p.has_time ? sizeof(float) * p.nb : 0;
   HSTU_DISPATCH(attn_fwd_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), dyn, s, P));
+                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), q_dyn_bytes(p), s, P));
   return hipGetLastError();
 }
 
@@ -890,9 +1005,8 @@ hipError_t launch_attn_dq_bf16(const AttnArgs &a, const void *dO, void *dq,
   P.out0 = (u16 *)dq;
   const Problem &p = a.p;
   const int grid = attn_dq_grid(p, current_dev());
-  const size_t dyn = p.has_time ? sizeof(float) * p.nb : 0;
   HSTU_DISPATCH(attn_dq_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), dyn, s, P));
+                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), q_dyn_bytes(p), s, P));
   return hipGetLastError();
 }
 
@@ -907,10 +1021,9 @@ hipError_t launch_attn_dkv_bf16(const AttnArgs &a, const void *dO, void *dk,
   P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
   P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
   const Problem &p = a.p;
-  const int grid = a.L.dkv_grid;   // the d_time partials are sized for it
-  const size_t dyn = p.has_time ? sizeof(float) * (size_t)p.nb * (p.H + 1) : 0;
+  const int grid = a.L.dkv_grid;
   HSTU_DISPATCH(attn_dkv_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), dyn, s, P));
+                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), k_dyn_bytes(p), s, P));
   return hipGetLastError();
 }
 

@@ -66,6 +66,17 @@ __device__ __forceinline__ int time_bucket(int64_t delta, int nb) {
   return b < nb - 1 ? b : nb - 1;
 }
 
+// Work-group barrier that orders LDS only: it waits for this wave's
+// outstanding LDS operations, not for its global loads, stores or atomics
+// (__syncthreads waits for those too).  For kernels whose threads exchange
+// data through LDS alone, so that fire-and-forget global atomics and
+// prefetch loads stay in flight across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // sigma(x) = 1 / (1 + e^-x) = 1 / (1 + 2^(-x log2 e)) in fp32 on the
 // hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32).  Saturates cleanly:
 // 2^(+large) = inf gives 0, 2^(-large) = 0 gives 1.

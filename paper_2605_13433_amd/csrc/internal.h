@@ -14,6 +14,11 @@ namespace hstu {
 // the work lists the scheduler builds.
 constexpr int TILE = 64;
 
+// The dK/dV work-groups fold their d_time histograms into this many partial
+// tables (work-group index mod DTIME_BINS) with float atomics; the finalize
+// kernel sums the bins in a fixed order.
+constexpr int DTIME_BINS = 16;
+
 // Control block at the head of every workspace (int32 words).
 enum CtrlSlot {
   CTRL_N_ENTRIES = 0,   // (sequence, tile) entries in each work list
@@ -62,6 +67,8 @@ const DeviceInfo &device_info(int dev);
 Layout make_layout(const Problem &p, bool for_bwd, int dev);
 
 // ---- launchers (each returns hipSuccess or the launch error) ----
+// Builds the work lists (and zeroes the d_time bins when the layout has
+// them, so the backward's later kernels can accumulate into them).
 hipError_t launch_schedule(const int64_t *seq_offsets, const Problem &p,
                            void *ws, const Layout &L, hipStream_t s);
 

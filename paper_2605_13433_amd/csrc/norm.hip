@@ -154,8 +154,9 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 //     offset m = N-1-x sums the per-sequence partials of every sequence
 //     longer than m.  Block = (h, 64 consecutive m); lane = m, waves stride
 //     over the sequences, then a cross-wave sum in LDS.
-//   d_time[h, k]: sum over work-groups of the dK/dV kernel's histograms.
-//     Block = 64 consecutive (h, k) columns; waves stride over the partials.
+//   d_time[h, k]: sum of the DTIME_BINS partial histograms the dK/dV
+//     work-groups folded theirs into.  Block = 64 consecutive (h, k)
+//     columns; waves stride over the bins.
 // Summation order is fixed, so the result is deterministic given the
 // partials.
 constexpr int FIN_THREADS = 512;
@@ -247,7 +248,7 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                      d_pos ? (const float *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
                      d_pos, pos_blocks,
                      d_time ? (const float *)(ws + a.L.dtime_part) : nullptr,
-                     a.L.dkv_grid, width, d_time);
+                     DTIME_BINS, width, d_time);
   return hipGetLastError();
 }
 

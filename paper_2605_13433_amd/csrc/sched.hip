@@ -31,7 +31,8 @@ __global__ void __launch_bounds__(SCHED_THREADS)
 schedule_kernel(const int64_t *__restrict__ off, int32_t B, int32_t N,
                 int64_t T, int32_t *__restrict__ ctrl,
                 SeqInfo *__restrict__ info, WorkEntry *__restrict__ list_q,
-                WorkEntry *__restrict__ list_k, int32_t nbins, int32_t cap) {
+                WorkEntry *__restrict__ list_k, int32_t nbins, int32_t cap,
+                float *__restrict__ zero_out, int32_t n_zero) {
   __shared__ int32_t count_ge[MAX_BINS];   // # sequences with ntiles == c
   __shared__ int32_t start[MAX_BINS];      // first slot of cost bin c
   __shared__ int32_t fill_q[MAX_BINS];
@@ -39,6 +40,7 @@ schedule_kernel(const int64_t *__restrict__ off, int32_t B, int32_t N,
   __shared__ int32_t total;
   const int tid = threadIdx.x;
 
+  for (int x = tid; x < n_zero; x += SCHED_THREADS) zero_out[x] = 0.0f;
   for (int c = tid; c < nbins; c += SCHED_THREADS) {
     count_ge[c] = 0;
     fill_q[c] = 0;
@@ -109,7 +111,9 @@ hipError_t launch_schedule(const int64_t *seq_offsets, const Problem &p,
                      (SeqInfo *)(base + L.seqinfo),
                      (WorkEntry *)(base + L.list_q),
                      L.list_k ? (WorkEntry *)(base + L.list_k) : nullptr, nbins,
-                     (int32_t)p.max_entries);
+                     (int32_t)p.max_entries,
+                     L.dtime_part ? (float *)(base + L.dtime_part) : nullptr,
+                     L.dtime_part ? DTIME_BINS * p.H * p.nb : 0);
   return hipGetLastError();
 }
 
