@@ -619,6 +619,10 @@ template <int D, bool POS>
 struct DkvSmem {
   StreamSmem<D> s;
   float shear[POS ? TILE * SHEAR_STRIDE : 1];
+  // d_pos of the current item by diagonal m = i - j, rolling over 128 slots
+  // (m & 127): a tile pair touches 127 consecutive diagonals, the next one
+  // shifts them by 64, so only completed diagonals leave for global memory
+  float dwin[POS ? 2 * TILE : 1];
   float kacc[KTAB];             // this item's d_time by float-exponent index
 };
 
@@ -639,6 +643,12 @@ attn_dkv_kernel(KParams P) {
     for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0f;
   }
   if (tid0 < 2) sm.flag[tid0] = 0;
+  if (POS) {
+    if (tid0 < 2 * TILE) smx.dwin[tid0] = 0.0f;
+    // positions (i, j - i + 63) with j outside the tile are never written
+    // again, so zero once: the column sums below read every row
+    for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
+  }
   int phase = 0;
 
   for (;;) {
@@ -825,19 +835,34 @@ attn_dkv_kernel(KParams P) {
         }
       }
       if (POS) {
-        // the diagonals of this tile pair are complete: sum column c (local
-        // offset j - i = c - 63) over one half of its rows and fold it into
-        // the sequence's d_pos partial (index m = i - j >= 0)
+        // column c of the sheared tile is diagonal m = (qt-kt)*64 - (c-63);
+        // sum its rows (independent loads; rows outside the tile hold 0),
+        // add it to the
+        // rolling window, and send diagonals no later tile touches
+        // (c >= 63, or every one on the item's last tile) to the sequence's
+        // d_pos partial
         lds_barrier();
-        const int c = tid & 127, half = tid >> 7;
+        const int c = tid;
         if (c < 2 * TILE - 1) {
-          const int lo = max(32 * half, TILE - 1 - c);
-          const int hi = min(32 * half + 32, 2 * TILE - 1 - c);
-          float val = 0.0f;
-          for (int i = lo; i < hi; ++i) val += smx.shear[i * SHEAR_STRIDE + c];
+          float v0 = 0.0f, v1 = 0.0f, v2 = 0.0f, v3 = 0.0f;
+#pragma unroll
+          for (int i = 0; i < TILE; i += 4) {
+            const float *col = smx.shear + i * SHEAR_STRIDE + c;
+            v0 += col[0];
+            v1 += col[SHEAR_STRIDE];
+            v2 += col[2 * SHEAR_STRIDE];
+            v3 += col[3 * SHEAR_STRIDE];
+          }
           const int m = (qt - kt) * TILE - (c - (TILE - 1));
-          if (val != 0.0f && m >= 0 && m < si.len)
-            atomicAdd(&P.dpos_part[(si.start + m) * P.H + h], val);
+          const int slot = m & (2 * TILE - 1);
+          const float acc = smx.dwin[slot] + ((v0 + v1) + (v2 + v3));
+          if (c >= TILE - 1 || qt + 1 == si.ntiles) {
+            smx.dwin[slot] = 0.0f;
+            if (acc != 0.0f && m >= 0 && m < si.len)
+              atomicAdd(&P.dpos_part[(si.start + m) * P.H + h], acc);
+          } else {
+            smx.dwin[slot] = acc;
+          }
         }
       }
     }
