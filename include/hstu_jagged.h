@@ -31,8 +31,9 @@
  * number of tokens, seq_offsets[B].
  *
  * Pointers.  Every tensor pointer is a DEVICE pointer on the current HIP
- * device; the caller owns all memory.  The library never allocates device
- * memory and never synchronises: each call enqueues its kernels on `stream`
+ * device; the caller owns all memory.  The attention calls never allocate
+ * device memory (for the layer calls see their section); no call
+ * synchronises: each call enqueues its kernels on `stream`
  * (a hipStream_t; NULL = the default stream) and returns.  Buffers must stay
  * alive until that work completes.
  *
@@ -137,6 +138,81 @@ size_t hstu_jagged_attn_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
                                         int32_t d, int64_t total_tokens,
                                         int32_t for_bwd, hstu_dtype dtype,
                                         const hstu_rab *rab);
+
+/* ---------------------------------------------------------------------------
+ * HSTU layer shell.  The attention above is the middle of one HSTU layer of
+ * the models the paper trains (HSTU / FuXi, Appendix A "Parameter Settings").
+ * These calls run a whole layer around it, with the library's reading of the
+ * layer (the paper does not spell it out): no input norm, residual, bias or
+ * dropout; SiLU on all of f1's output; split order U, V, Q, K.
+ *
+ *   h   = x . w1                       f1 GEMM      [T][4*H*d]
+ *   z   = silu(h)  split by columns     U | V | Q | K, each [T][H][d]
+ *   y   = LayerNorm(attention(q, k, v) ) * u        as hstu_jagged_attn_fwd
+ *   out = y . w2                       f2 GEMM      [T][d_model]
+ *
+ * and the backward of sum(out * dout) into dx, dw1, dw2 and the table
+ * gradients.  The GEMMs run on hipBLASLt (bf16 in and out, float32
+ * accumulation); silu and the split run in one library kernel, its
+ * derivative and the merge back in another.  HSTU_BF16 only, d in {64, 128},
+ * 1 <= d_model <= 65536 and d_model % 8 == 0.  Weights are row-major:
+ * w1 [d_model][4*H*d], w2 [H*d][d_model]; x, out, dx [T][d_model].
+ *
+ * Allocation: the first layer call on a device creates that device's
+ * hipBLASLt handle (hipBLASLt may allocate its own state then) and each new
+ * GEMM shape runs one algorithm query; both are cached for the process.
+ * GEMM scratch comes from the caller's workspace.  Thread-safe.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    hstu_dtype dtype;            /* HSTU_BF16                                */
+    int64_t total_tokens;        /* T = seq_offsets[B]                       */
+    void *out;                   /* [T][d_model]  y . w2                     */
+    void *h;                     /* [T][4*H*d]    x . w1 (saved)             */
+    void *z;                     /* [4][T][H][d]  silu(h) as planes U,V,Q,K
+                                    (saved; the attention's u, v, q, k)      */
+    void *y;                     /* [T][H*d]      LayerNorm(o) * u (saved)   */
+    void *o;                     /* [T][H][d]     (saved)                    */
+    float *ln_mean;              /* [T]           (saved)                    */
+    float *ln_rstd;              /* [T]           (saved)                    */
+    void *workspace;             /* device scratch, 256-byte aligned         */
+    size_t workspace_bytes;      /* >= hstu_layer_workspace_bytes(..,0)      */
+} hstu_layer_fwd_out;
+
+typedef struct {
+    hstu_dtype dtype;            /* HSTU_BF16                                */
+    int64_t total_tokens;
+    const void *dout;            /* [T][d_model]                             */
+    const void *h, *z, *y, *o;   /* saved by hstu_layer_fwd                  */
+    const float *ln_mean, *ln_rstd;
+    void *dx;                    /* [T][d_model]        overwritten          */
+    void *dw1;                   /* [d_model][4*H*d]    overwritten          */
+    void *dw2;                   /* [H*d][d_model]      overwritten          */
+    float *d_pos_w;              /* as in hstu_bwd_io                        */
+    float *d_time_w;
+    void *workspace;             /* device scratch, 256-byte aligned         */
+    size_t workspace_bytes;      /* >= hstu_layer_workspace_bytes(..,1)      */
+} hstu_layer_bwd_io;
+
+/* Layer forward: out and the saved state from x, w1, w2.  T = 0 enqueues
+ * nothing. */
+int hstu_layer_fwd(const void *x, const void *w1, const void *w2,
+                   const int64_t *seq_offsets, int32_t B, int32_t max_len,
+                   int32_t H, int32_t d, int32_t d_model, const hstu_rab *rab,
+                   hstu_layer_fwd_out *out, void *stream);
+
+/* Layer backward: dx, dw1, dw2, d_pos_w, d_time_w of sum(out * dout).  With
+ * T = 0 the weight and table gradients are written as zeros. */
+int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
+                   const int64_t *seq_offsets, int32_t B, int32_t max_len,
+                   int32_t H, int32_t d, int32_t d_model, const hstu_rab *rab,
+                   hstu_layer_bwd_io *io, void *stream);
+
+/* Workspace bytes of a layer forward (for_bwd = 0) or backward call; 0 for
+ * invalid sizes. */
+size_t hstu_layer_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
+                                  int32_t d, int32_t d_model,
+                                  int64_t total_tokens, int32_t for_bwd,
+                                  hstu_dtype dtype, const hstu_rab *rab);
 
 /* Runs only the seq_offsets tile scheduler (the first step of both calls)
  * and copies its work lists out, for inspection and tests.  Work is split

@@ -1,6 +1,6 @@
 """Builds libhstu_jagged.so (HIP kernels + C ABI) for gfx950, in-tree.
 
-Every HIP translation unit is compiled by hipcc with packed fp32 vector ops
+Every translation unit is compiled by hipcc with packed fp32 vector ops
 disabled (-Xclang -target-feature -Xclang -packed-fp32-ops) and with
 hardware float atomics on device memory (-munsafe-fp-atomics), then linked
 into one shared library next to this file.
@@ -17,13 +17,18 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhstu_jagged.so")
 ARCH = "gfx950"
-SOURCES = ["api.cpp", "sched.hip", "attn_bf16.hip", "attn_f32.hip", "norm.hip"]
+SOURCES = ["api.cpp", "sched.hip", "attn_bf16.hip", "attn_f32.hip", "norm.hip",
+           "layer.cpp", "layer_kernels.hip"]
 HEADERS = ["device.h", "internal.h"]
 
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-munsafe-fp-atomics", "-Wall", "-Wno-unused-function",
           "-Wno-unused-variable"]
+
+
+# The layer shell's GEMMs run on hipBLASLt.
+LDFLAGS = ["-L/opt/rocm/lib", "-lhipblaslt"]
 
 
 def _hipcc() -> str:
@@ -49,7 +54,8 @@ def build(verbose: bool = False) -> str:
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs,
+           *LDFLAGS, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stderr}")

@@ -15,11 +15,9 @@
 #include "internal.h"
 
 namespace hstu {
-namespace {
 
 thread_local std::string g_last_error;
 
-int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char *fmt, ...) {
   char buf[512];
   va_list ap;
@@ -30,14 +28,15 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
+void clear_last_error() { g_last_error.clear(); }
+
 int hip_fail(hipError_t e, const char *what) {
   return fail(HSTU_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr size_t kAlign = 256;
-size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
+namespace {
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+}  // namespace
 
 // Validates everything the host can see; on success fills `p`.
 int validate(const void *q, const void *k, const void *v, const void *u,
@@ -81,14 +80,20 @@ int validate(const void *q, const void *k, const void *v, const void *u,
   return HSTU_OK;
 }
 
-int check_workspace(const Layout &L, void *ws, size_t bytes) {
-  if (!ws) return fail(HSTU_EWORKSPACE, "workspace is NULL (%zu bytes needed)", L.total);
+int check_workspace_bytes(size_t need, void *ws, size_t bytes) {
+  if (!ws) return fail(HSTU_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);
   if ((uintptr_t)ws % kAlign)
     return fail(HSTU_EINVAL, "workspace is not %zu-byte aligned", kAlign);
-  if (bytes < L.total)
-    return fail(HSTU_EWORKSPACE, "workspace has %zu bytes, %zu needed", bytes, L.total);
+  if (bytes < need)
+    return fail(HSTU_EWORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
   return HSTU_OK;
 }
+
+namespace {
+int check_workspace(const Layout &L, void *ws, size_t bytes) {
+  return check_workspace_bytes(L.total, ws, bytes);
+}
+}  // namespace
 
 int current_device(int *dev) {
   hipError_t e = hipGetDevice(dev);
@@ -96,9 +101,8 @@ int current_device(int *dev) {
   return HSTU_OK;
 }
 
-// Optional per-kernel timing: events recorded around each launch on the
-// launch stream (see hstu_profile_enable).
 namespace prof {
+namespace {
 struct Rec {
   const char *name;
   hipEvent_t a, b;
@@ -118,34 +122,30 @@ hipEvent_t take_event() {
   return hipEventCreate(&e) == hipSuccess ? e : nullptr;
 }
 
-struct Scope {
-  const char *name;
-  hipStream_t s;
-  hipEvent_t a = nullptr;
-  Scope(const char *n, hipStream_t st) : name(n), s(st) {
-    if (!on.load(std::memory_order_relaxed)) return;
-    std::lock_guard<std::mutex> lock(mu);
-    a = take_event();
-    if (a && hipEventRecord(a, s) != hipSuccess) {
-      pool.push_back(a);
-      a = nullptr;
-    }
-  }
-  ~Scope() {
-    if (!a) return;
-    std::lock_guard<std::mutex> lock(mu);
-    hipEvent_t b = take_event();
-    if (b && hipEventRecord(b, s) == hipSuccess) {
-      recs.push_back(Rec{name, a, b});
-    } else {
-      pool.push_back(a);
-      if (b) pool.push_back(b);
-    }
-  }
-};
-}  // namespace prof
-
 }  // namespace
+
+Scope::Scope(const char *n, hipStream_t st) : name(n), s(st) {
+  if (!on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lock(mu);
+  a = take_event();
+  if (a && hipEventRecord(a, s) != hipSuccess) {
+    pool.push_back(a);
+    a = nullptr;
+  }
+}
+
+Scope::~Scope() {
+  if (!a) return;
+  std::lock_guard<std::mutex> lock(mu);
+  hipEvent_t b = take_event();
+  if (b && hipEventRecord(b, s) == hipSuccess) {
+    recs.push_back(Rec{name, a, b});
+  } else {
+    pool.push_back(a);
+    if (b) pool.push_back(b);
+  }
+}
+}  // namespace prof
 
 const DeviceInfo &device_info(int dev) {
   static std::mutex mu;

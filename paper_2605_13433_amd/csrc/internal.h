@@ -58,6 +58,34 @@ struct Layout {
   int dkv_grid;          // persistent grid of the dK/dV kernel (WG count)
 };
 
+// ---- host helpers shared by the C-ABI translation units ----
+// Records a formatted message as the thread's last error; returns `code`.
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_last_error();
+int hip_fail(hipError_t e, const char *what);
+int current_device(int *dev);
+// Validates every host-visible argument of an attention call; fills `p`.
+int validate(const void *q, const void *k, const void *v, const void *u,
+             const int64_t *off, int32_t B, int32_t N, int32_t H, int32_t d,
+             const hstu_rab *rab, hstu_dtype dtype, int64_t T, Problem *p);
+// Workspace pointer non-null, 256-byte aligned and at least `need` bytes.
+int check_workspace_bytes(size_t need, void *ws, size_t bytes);
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Optional per-kernel timing (hstu_profile_enable): a Scope brackets one
+// launch with two HIP events recorded on the launch stream.
+namespace prof {
+struct Scope {
+  const char *name;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  Scope(const char *n, hipStream_t st);
+  ~Scope();
+};
+}  // namespace prof
+
 // Device properties the launch shapes depend on (cached per device).
 struct DeviceInfo {
   int num_cu;
@@ -99,6 +127,16 @@ hipError_t launch_ln_bwd(const Problem &p, const void *dy, const void *u,
                          void *du, void *dO, float *dpos_part, hipStream_t s);
 hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                                   float *d_time, hipStream_t s);
+
+// HSTU layer shell pointwise passes; C = H*d (a multiple of 64).
+// z planes [4][T][C] = silu(h [T][4C]) split by column blocks.
+hipError_t launch_silu_split(const void *h, void *z, int64_t T, int32_t C,
+                             int dev, hipStream_t s);
+// dh [T][4C] = dz planes * silu'(h).
+hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
+                              int64_t T, int32_t C, int dev, hipStream_t s);
+// Zero `bytes` (a multiple of 4) of device memory with a kernel.
+hipError_t launch_zero(void *p, size_t bytes, int dev, hipStream_t s);
 
 // Persistent-grid sizes (work-groups) of the bf16 attention kernels.
 int attn_fwd_grid(const Problem &p, int dev);

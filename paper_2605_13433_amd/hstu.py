@@ -1,4 +1,5 @@
-"""Python binding of the jagged HSTU attention C ABI (include/hstu_jagged.h).
+"""Python binding of the jagged HSTU attention C ABI (include/hstu_jagged.h),
+including the HSTU layer shell calls.
 
 Argument marshalling only: every step of the computation runs in the HIP
 kernels of libhstu_jagged.so.  PyTorch supplies device memory and the
@@ -53,6 +54,24 @@ class BwdIO(ctypes.Structure):
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
+class LayerFwdOut(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("total_tokens", ctypes.c_int64),
+                ("out", ctypes.c_void_p), ("h", ctypes.c_void_p), ("z", ctypes.c_void_p),
+                ("y", ctypes.c_void_p), ("o", ctypes.c_void_p),
+                ("ln_mean", ctypes.c_void_p), ("ln_rstd", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class LayerBwdIO(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("total_tokens", ctypes.c_int64),
+                ("dout", ctypes.c_void_p), ("h", ctypes.c_void_p), ("z", ctypes.c_void_p),
+                ("y", ctypes.c_void_p), ("o", ctypes.c_void_p),
+                ("ln_mean", ctypes.c_void_p), ("ln_rstd", ctypes.c_void_p),
+                ("dx", ctypes.c_void_p), ("dw1", ctypes.c_void_p), ("dw2", ctypes.c_void_p),
+                ("d_pos_w", ctypes.c_void_p), ("d_time_w", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
 _lib = None
 
 
@@ -77,6 +96,15 @@ def load_library(path: str = LIB_PATH):
     lib.hstu_jagged_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.hstu_jagged_schedule.argtypes = [P, i32, i32, i64, P, P, P, P, ctypes.c_size_t, P]
     lib.hstu_jagged_schedule.restype = ctypes.c_int
+    lib.hstu_layer_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32,
+                                   ctypes.POINTER(Rab), ctypes.POINTER(LayerFwdOut), P]
+    lib.hstu_layer_fwd.restype = ctypes.c_int
+    lib.hstu_layer_bwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32,
+                                   ctypes.POINTER(Rab), ctypes.POINTER(LayerBwdIO), P]
+    lib.hstu_layer_bwd.restype = ctypes.c_int
+    lib.hstu_layer_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i64, i32,
+                                               ctypes.c_int, ctypes.POINTER(Rab)]
+    lib.hstu_layer_workspace_bytes.restype = ctypes.c_size_t
     lib.hstu_last_error.argtypes = []
     lib.hstu_last_error.restype = ctypes.c_char_p
     lib.hstu_version.argtypes = []
@@ -152,6 +180,32 @@ def hstu_jagged_schedule(seq_offsets, B, max_len, total_tokens, n_entries, list_
     _check(load_library().hstu_jagged_schedule(
         _ptr(seq_offsets), int(B), int(max_len), int(total_tokens), _ptr(n_entries),
         _ptr(list_q), _ptr(list_k), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def hstu_layer_workspace_bytes(B, max_len, H, d, d_model, total_tokens, for_bwd,
+                               dtype_code, rab: Optional[Rab] = None) -> int:
+    n = load_library().hstu_layer_workspace_bytes(
+        int(B), int(max_len), int(H), int(d), int(d_model), int(total_tokens),
+        int(for_bwd), int(dtype_code), ctypes.byref(rab) if rab is not None else None)
+    if n == 0:
+        raise HstuError(-1, last_error())
+    return n
+
+
+def hstu_layer_fwd(x, w1, w2, seq_offsets, B, max_len, H, d, d_model,
+                   rab: Optional[Rab], out: LayerFwdOut, stream=None) -> None:
+    _check(load_library().hstu_layer_fwd(
+        _ptr(x), _ptr(w1), _ptr(w2), _ptr(seq_offsets), int(B), int(max_len), int(H),
+        int(d), int(d_model), ctypes.byref(rab) if rab is not None else None,
+        ctypes.byref(out), _stream(stream)))
+
+
+def hstu_layer_bwd(x, w1, w2, seq_offsets, B, max_len, H, d, d_model,
+                   rab: Optional[Rab], io: LayerBwdIO, stream=None) -> None:
+    _check(load_library().hstu_layer_bwd(
+        _ptr(x), _ptr(w1), _ptr(w2), _ptr(seq_offsets), int(B), int(max_len), int(H),
+        int(d), int(d_model), ctypes.byref(rab) if rab is not None else None,
+        ctypes.byref(io), _stream(stream)))
 
 
 def max_entries(B: int, max_len: int, total_tokens: int) -> int:
@@ -262,3 +316,80 @@ def forward_backward(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=No
     f = plan.forward(q, k, v, u, seq_offsets)
     g = plan.backward(q, k, v, u, seq_offsets, dy)
     return f, g
+
+
+# ------------------------------------------------------------ layer shell
+@dataclass
+class LayerFwdResult:
+    out: torch.Tensor       # [T, d_model]
+    h: torch.Tensor         # [T, 4*H*d]   x . w1
+    z: torch.Tensor         # [4, T, H, d] silu(h) planes U, V, Q, K
+    y: torch.Tensor         # [T, H*d]
+    o: torch.Tensor         # [T, H, d]
+    ln_mean: torch.Tensor
+    ln_rstd: torch.Tensor
+
+
+@dataclass
+class LayerBwdResult:
+    dx: torch.Tensor
+    dw1: torch.Tensor
+    dw2: torch.Tensor
+    d_pos_w: Optional[torch.Tensor]
+    d_time_w: Optional[torch.Tensor]
+
+
+class LayerPlan:
+    """Saved state, gradients and workspaces of one HSTU layer shape."""
+
+    def __init__(self, x, seq_offsets, max_len, H, d, pos_w=None, time_w=None,
+                 timestamps=None, num_buckets=128, backward=True):
+        T, D = x.shape
+        dev = x.device
+        self.B = seq_offsets.numel() - 1
+        self.N, self.H, self.d, self.D, self.T = int(max_len), int(H), int(d), int(D), T
+        C = H * d
+        self.rab = make_rab(pos_w, time_w, timestamps, num_buckets)
+        self._keep = (pos_w, time_w, timestamps)
+        code = _dtype_code(x)
+        self.fwd_ws = _workspace(hstu_layer_workspace_bytes(
+            self.B, self.N, H, d, D, T, 0, code, self.rab), dev)
+        bf = dict(dtype=x.dtype, device=dev)
+        self.res = LayerFwdResult(
+            out=torch.empty(T, D, **bf), h=torch.empty(T, 4 * C, **bf),
+            z=torch.empty(4, T, H, d, **bf), y=torch.empty(T, C, **bf),
+            o=torch.empty(T, H, d, **bf),
+            ln_mean=torch.empty(T, dtype=torch.float32, device=dev),
+            ln_rstd=torch.empty(T, dtype=torch.float32, device=dev))
+        r = self.res
+        self.out = LayerFwdOut(code, T, _ptr(r.out), _ptr(r.h), _ptr(r.z), _ptr(r.y),
+                               _ptr(r.o), _ptr(r.ln_mean), _ptr(r.ln_rstd),
+                               _ptr(self.fwd_ws), self.fwd_ws.numel())
+        self.io = None
+        if backward:
+            self.bwd_ws = _workspace(hstu_layer_workspace_bytes(
+                self.B, self.N, H, d, D, T, 1, code, self.rab), dev)
+            self.grad = LayerBwdResult(
+                dx=torch.empty(T, D, **bf), dw1=torch.empty(D, 4 * C, **bf),
+                dw2=torch.empty(C, D, **bf),
+                d_pos_w=(torch.empty(H, 2 * self.N - 1, dtype=torch.float32, device=dev)
+                         if pos_w is not None else None),
+                d_time_w=(torch.empty(H, num_buckets, dtype=torch.float32, device=dev)
+                          if time_w is not None else None))
+            g = self.grad
+            self.io = LayerBwdIO(code, T, None, _ptr(r.h), _ptr(r.z), _ptr(r.y), _ptr(r.o),
+                                 _ptr(r.ln_mean), _ptr(r.ln_rstd), _ptr(g.dx), _ptr(g.dw1),
+                                 _ptr(g.dw2), _ptr(g.d_pos_w), _ptr(g.d_time_w),
+                                 _ptr(self.bwd_ws), self.bwd_ws.numel())
+
+    def forward(self, x, w1, w2, seq_offsets, stream=None) -> LayerFwdResult:
+        hstu_layer_fwd(x, w1, w2, seq_offsets, self.B, self.N, self.H, self.d, self.D,
+                       self.rab, self.out, stream)
+        return self.res
+
+    def backward(self, x, w1, w2, seq_offsets, dout, stream=None) -> LayerBwdResult:
+        self.io.dout = _ptr(dout)
+        self._dout = dout
+        hstu_layer_bwd(x, w1, w2, seq_offsets, self.B, self.N, self.H, self.d, self.D,
+                       self.rab, self.io, stream)
+        return self.grad

@@ -202,9 +202,13 @@ def subset(w: Workload, seqs) -> Workload:
     offsets = np.zeros(len(seqs) + 1, dtype=np.int64)
     np.cumsum(lengths, out=offsets[1:])
     pick = lambda t: None if t is None else t.index_select(0, rows_t)
+    extra = {}
+    if "x" in w.extra:   # layer inputs: token rows follow, weights are shared
+        extra = dict(x=pick(w.extra["x"]), w1=w.extra["w1"], w2=w.extra["w2"],
+                     dout=pick(w.extra.get("dout")))
     return Workload(B=len(seqs), H=w.H, d=w.d, N=w.N, dtype=w.dtype,
                     lengths=lengths, seq_offsets=torch.from_numpy(offsets),
                     q=pick(w.q), k=pick(w.k), v=pick(w.v), u=pick(w.u),
                     dy=pick(w.dy), pos_w=w.pos_w, time_w=w.time_w,
                     timestamps=pick(w.timestamps), num_buckets=w.num_buckets,
-                    name=w.name + "[subset]", extra={})
+                    name=w.name + "[subset]", extra=extra)

@@ -100,3 +100,57 @@ def test_workspace_query_rejects_bad_sizes():
     lib = hstu.load_library()
     assert lib.hstu_jagged_attn_workspace_bytes(2, 64, 2, 48, 10, 0, 0, None) == 0
     assert "d = 48" in hstu.last_error()
+
+
+def _layer_fwd(B=2, N=64, H=2, d=64, D=128, dtype=hstu.HSTU_BF16, T=10, null=()):
+    p = {n: (None if n in null else FAKE) for n in ("x", "w1", "w2", "off", "z", "out")}
+    out = hstu.LayerFwdOut(dtype, T, p["out"], FAKE, p["z"], FAKE, FAKE, FAKE, FAKE,
+                           FAKE, 1 << 40)
+    return hstu.load_library().hstu_layer_fwd(p["x"], p["w1"], p["w2"], p["off"], B, N, H,
+                                              d, D, None, ctypes.byref(out), None)
+
+
+@pytest.mark.parametrize("kw,code,frag", [
+    (dict(dtype=hstu.HSTU_F32), -2, "HSTU_BF16 only"),
+    (dict(D=12), -1, "d_model = 12"),
+    (dict(D=0), -1, "d_model = 0"),
+    (dict(D=65544), -1, "d_model"),
+    (dict(d=32), -2, "bf16"),
+    (dict(H=0), -1, "H = 0"),
+    (dict(null=("x",)), -1, "x, w1 and w2"),
+    (dict(null=("w2",)), -1, "x, w1 and w2"),
+    (dict(null=("z",)), -1, "non-null"),
+    (dict(null=("out",)), -1, "out->out"),
+    (dict(null=("x", "w1", "w2", "z", "out"), T=0), 0, ""),
+])
+def test_layer_fwd_validation(kw, code, frag):
+    assert _layer_fwd(**kw) == code
+    assert frag in hstu.last_error()
+
+
+def test_layer_bwd_validation():
+    lib = hstu.load_library()
+    io = hstu.LayerBwdIO(hstu.HSTU_BF16, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                         FAKE, None, FAKE, None, None, FAKE, 1 << 40)
+    rc = lib.hstu_layer_bwd(FAKE, FAKE, FAKE, FAKE, 2, 64, 2, 64, 128, None,
+                            ctypes.byref(io), None)
+    assert rc == -1 and "dw1" in hstu.last_error()
+    io.dw1 = FAKE
+    r = hstu.Rab(FAKE, None, None, 0)
+    rc = lib.hstu_layer_bwd(FAKE, FAKE, FAKE, FAKE, 2, 64, 2, 64, 128, ctypes.byref(r),
+                            ctypes.byref(io), None)
+    assert rc == -1 and "d_pos_w" in hstu.last_error()
+    io.dx = None
+    rc = lib.hstu_layer_bwd(FAKE, FAKE, FAKE, FAKE, 2, 64, 2, 64, 128, None,
+                            ctypes.byref(io), None)
+    assert rc == -1 and "dx" in hstu.last_error()
+    assert lib.hstu_layer_bwd(FAKE, FAKE, FAKE, FAKE, 2, 64, 2, 64, 128, None,
+                              None, None) == -1
+
+
+def test_layer_workspace_query_rejects_bad_sizes():
+    lib = hstu.load_library()
+    assert lib.hstu_layer_workspace_bytes(2, 64, 2, 64, 100, 10, 1, 0, None) == 0
+    assert "d_model = 100" in hstu.last_error()
+    assert lib.hstu_layer_workspace_bytes(2, 64, 2, 64, 128, 10, 0, 1, None) == 0
+    assert "HSTU_BF16" in hstu.last_error()
