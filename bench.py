@@ -10,6 +10,10 @@ L_b (L_b + 1) / 2 causal pairs per head (forward 4 d H P for QK^T and AV,
 backward 8 d H P for dA, dV, dQ, dK; recompute, bias, SiLU and LayerNorm
 work are not credited; padding does not exist).  Prints one JSON line.
 
+With the layer workload (--workload 4) the line also carries a "layer"
+object: the whole HSTU layer around the attention (f1/f2 GEMMs, SiLU split
+and their backward) timed the same way.
+
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
 """
 from __future__ import annotations
@@ -92,7 +96,80 @@ def load_traffic(kernel: str, workload: str, sha: str):
     return (fetch * scale_f + write * scale_w) * 1024.0
 
 
-def cpu_baseline(w, target_s=15.0):
+def read_kernel_profile(lib):
+    """Per-kernel averages from the library's event profiler (same stream)."""
+    import ctypes
+    nmax = 32
+    names = (ctypes.c_char_p * nmax)()
+    tot = (ctypes.c_double * nmax)()
+    cnt = (ctypes.c_int * nmax)()
+    lib.hstu_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
+                                      ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_int)]
+    rows = lib.hstu_profile_read(nmax, names, tot, cnt)
+    return {names[i].decode(): {"avg_us": 1e3 * tot[i] / cnt[i], "launches": cnt[i]}
+            for i in range(max(rows, 0))}
+
+
+def layer_bench(lib, w, steps, warmup, stream):
+    """The full HSTU layer (f1 GEMM, SiLU split, attention + LN*U, f2 GEMM,
+    and the backward through all of them) on the same batch: step time,
+    credited flops (six GEMMs + the attention's 12 d H P) and per-kernel
+    times, GEMMs with their TFLOP/s against the bf16 MFMA peak."""
+    import torch
+    from paper_2605_13433_amd import hstu
+    e = w.extra
+    dev = lambda t: None if t is None else t.contiguous().cuda()
+    x, w1, w2, off, dout = (dev(t) for t in (e["x"], e["w1"], e["w2"], w.seq_offsets,
+                                             e["dout"]))
+    pos, tw, ts = dev(w.pos_w), dev(w.time_w), dev(w.timestamps)
+    plan = hstu.LayerPlan(x, off, w.N, w.H, w.d, pos, tw, ts, w.num_buckets)
+
+    def step():
+        plan.forward(x, w1, w2, off, stream)
+        plan.backward(x, w1, w2, off, dout, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        step()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    lib.hstu_profile_enable(1)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    lib.hstu_profile_enable(0)
+    kernels = read_kernel_profile(lib)
+    T, D, C = w.T, x.shape[1], w.H * w.d
+    big, small = 2.0 * T * D * 4 * C, 2.0 * T * C * D
+    gemm_flops = {"gemm_f1": big, "gemm_f2": small, "gemm_dy": small,
+                  "gemm_dw2": small, "gemm_dx": big, "gemm_dw1": big}
+    for n, r in kernels.items():
+        if n in gemm_flops:
+            r["TFLOP_s"] = round(gemm_flops[n] / (r["avg_us"] * 1e-6) / 1e12, 1)
+            r["frac_of_bf16_peak"] = round(r["TFLOP_s"] / PEAK_BF16_TFLOPS, 4)
+        r["avg_us"] = round(r["avg_us"], 2)
+    attn = 12.0 * w.d * w.H * w.pairs
+    g = sum(gemm_flops.values())
+    return {
+        "ms_per_step": round(ms, 5),
+        "credited_flops": g + attn,
+        "gemm_flops": g,
+        "attention_flops": attn,
+        "TFLOP_s": round((g + attn) / (ms * 1e-3) / 1e12, 2),
+        "pct_of_bf16_peak": round(100.0 * (g + attn) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 3),
+        "d_model": int(D),
+        "kernels": kernels,
+    }
+
+
+def cpu_baseline(w, target_s=20.0):
     """The oracle, as it stands, on a bounded sample of the same workload:
     whole sequences in a seeded random order until the estimated
     forward+backward time reaches `target_s`."""
@@ -220,23 +297,12 @@ def main():
     value = flops_step / (ms_per_step * 1e-3) / 1e12
 
     # ---- per-kernel durations: HIP events around every launch, same stream
-    import ctypes
     lib.hstu_profile_enable(1)
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     lib.hstu_profile_enable(0)
-    nmax = 32
-    names = (ctypes.c_char_p * nmax)()
-    tot = (ctypes.c_double * nmax)()
-    cnt = (ctypes.c_int * nmax)()
-    lib.hstu_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
-                                      ctypes.POINTER(ctypes.c_double),
-                                      ctypes.POINTER(ctypes.c_int)]
-    rows = lib.hstu_profile_read(nmax, names, tot, cnt)
-    kernels = {}
-    for i in range(max(rows, 0)):
-        kernels[names[i].decode()] = {"avg_us": 1e3 * tot[i] / cnt[i], "launches": cnt[i]}
+    kernels = read_kernel_profile(lib)
 
     # ---- cold cache: flush L2 + MALL (1 GiB of writes) before each step
     cold_ms = None
@@ -311,6 +377,8 @@ def main():
         "roofline": roof,
         "kernel_source_sha": sha,
     }
+    if "x" in w.extra:
+        out["layer"] = layer_bench(lib, w, args.steps, args.warmup, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out))
