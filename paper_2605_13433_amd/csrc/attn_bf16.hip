@@ -66,6 +66,7 @@ struct KParams {
   float *dpos_part, *dtime_part;
   int32_t H, N, nb;
   float inv_n;
+  int32_t all_heads;      // time tables of every head staged once per work-group
 };
 
 // ------------------------------------------------------------ tile staging
@@ -207,10 +208,27 @@ struct StreamSmem {
   alignas(16) float pos[4 * POS_COPY];
   alignas(16) int32_t ts32[TILE];        // streamed-tile timestamps - ts_start
   int64_t ts64[TILE];                    // raw streamed-tile timestamps
-  float ktab[KTAB];                      // float-exponent index -> time bias
   int flag[2];                           // "some timestamp is far" (parity-buffered)
   int item;
 };
+
+// d_time is accumulated in LDS as 64-bit fixed point (value * 2^24) with
+// integer atomics: LDS float atomics cost hundreds of cycles per wave
+// instruction here, integer ones do not.  Range: each added run sum below
+// 2^31 in magnitude and each work-group partial below 2^39; resolution
+// 2^-24 (6e-8) per added run.
+typedef unsigned long long fix64;
+
+__device__ __forceinline__ fix64 to_fixed(float v) {
+  const float fl = __builtin_floorf(v);
+  const int hi = (int)fl;                                   // saturating cvt
+  const unsigned lo = (unsigned)((v - fl) * 16777216.0f);   // [0, 2^24]
+  return (fix64)(((long long)hi << 24) + (long long)lo);
+}
+
+__device__ __forceinline__ float from_fixed(fix64 v) {
+  return (float)((double)(long long)v * (1.0 / 16777216.0));
+}
 
 // Per-lane running sum of d_time contributions over one time index (the
 // lane's pairs visit non-decreasing indices when timestamps are ordered, so
@@ -218,28 +236,93 @@ struct StreamSmem {
 struct TimeRun {
   float sum = 0.0f;
   int cur = -1;
-  __device__ __forceinline__ void add(float *acc, int k, float v) {
+  __device__ __forceinline__ void add(fix64 *acc, int k, float v) {
     if (k != cur) {
-      if (cur >= 0) atomicAdd(&acc[cur], sum);
+      if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
       cur = k;
       sum = 0.0f;
     }
     sum += v;
   }
-  __device__ __forceinline__ void flush(float *acc) {
-    if (cur >= 0) atomicAdd(&acc[cur], sum);
+  __device__ __forceinline__ void flush(fix64 *acc) {
+    if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
     cur = -1;
     sum = 0.0f;
   }
 };
 
-// Item-level set-up shared by the kernels: time tables of head h.
-template <int D>
-__device__ __forceinline__ void stage_time_tables(const KParams &P, StreamSmem<D> &sm,
-                                                  float *tw, int h, int tid) {
+
+// Time tables in dynamic LDS, one slot per head (or a single slot restaged
+// per item when all heads do not fit): KTAB entries by float-exponent index,
+// then the nb raw buckets for the exact path.
+__device__ __forceinline__ int time_slot_floats(const KParams &P) { return KTAB + P.nb; }
+
+__device__ __forceinline__ void stage_time_head(const KParams &P, float *slot, int h, int tid) {
   const float *tab = P.time_w + (int64_t)h * P.nb;
-  for (int x = tid; x < P.nb; x += THREADS) tw[x] = tab[x];
-  for (int x = tid; x < KTAB; x += THREADS) sm.ktab[x] = tab[bucket_of_index(x, P.nb)];
+  for (int x = tid; x < KTAB; x += THREADS) slot[x] = tab[bucket_of_index(x, P.nb)];
+  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = tab[x];
+}
+
+// Kernel start: every head's tables when they fit (then no per-item staging).
+__device__ __forceinline__ void stage_all_heads(const KParams &P, float *dyn, int tid) {
+  if (!P.all_heads) return;
+  for (int h = 0; h < P.H; ++h) stage_time_head(P, dyn + h * time_slot_floats(P), h, tid);
+}
+
+// Item start: the slot of head h (staged now if tables are per item).
+__device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, int h, int tid) {
+  if (P.all_heads) return dyn + h * time_slot_floats(P);
+  stage_time_head(P, dyn, h, tid);
+  return dyn;
+}
+
+// Cross-wave sum of a 64 x D fp32 output tile and its coalesced bf16 store.
+// The two waves of each stationary row half hold partial sums over the two
+// halves of the streamed side, in accumulator layout (rows 32*half +
+// c_row(r, g), columns 32*db + l32).  The writer wave stores its blocks to
+// LDS, its partner adds its own in place, then every thread converts 8
+// consecutive floats of one
+// row and writes them as a single 16-byte chunk; rows at or beyond `valid`
+// are not written.  (The partner reads, adds and writes back its own
+// addresses: LDS float atomics are far slower here even without conflicts.)
+template <int D>
+__device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D / 32],
+                                               bool writer, int half, int g, int l32,
+                                               int tid, u16 *__restrict__ out,
+                                               int row_stride, int valid) {
+  lds_barrier();
+  if (writer) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(32 * half + c_row(r, g)) * D + 32 * db + l32] = acc[db][r];
+  }
+  lds_barrier();
+  if (!writer) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(32 * half + c_row(r, g)) * D + 32 * db + l32] += acc[db][r];
+  }
+  lds_barrier();
+  constexpr int CH = TILE * D / 8 / THREADS;
+#pragma unroll
+  for (int x = 0; x < CH; ++x) {
+    const int ch = tid + THREADS * x;
+    const int row = ch / (D / 8), c8 = ch % (D / 8);
+    if (row < valid) {
+      const float4 a = *(const float4 *)(red + row * D + 8 * c8);
+      const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
+      uint4 pk;
+      pk.x = pack2(a.x, a.y);
+      pk.y = pack2(a.z, a.w);
+      pk.z = pack2(b.x, b.y);
+      pk.w = pack2(b.z, b.w);
+      *(uint4 *)(out + row * row_stride + 8 * c8) = pk;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- forward
@@ -247,11 +330,12 @@ template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, 2)
 attn_fwd_kernel(KParams P) {
   __shared__ StreamSmem<D> sm;
-  extern __shared__ float tw[];               // time_w row of the item's head
+  extern __shared__ float dyn[];              // time tables (see item_time_slot)
   constexpr int ST = D + RM_PAD;
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
   if (tid0 < 2) sm.flag[tid0] = 0;
+  if (TIME) stage_all_heads(P, dyn, tid0);
   int phase = 0;
 
   for (;;) {
@@ -284,13 +368,14 @@ attn_fwd_kernel(KParams P) {
     int64_t ts_start = 0, ts_i = 0;
     int32_t ts_i32 = 0;
     bool q_far = false;
+    float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      stage_time_tables<D>(P, sm, tw, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid);
     }
 
     f32x16 oacc[D / 32];
@@ -363,15 +448,15 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
             const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
-            x[4 * q4 + 0] += sm.ktab[time_index(ts_i32 - t4.x)];
-            x[4 * q4 + 1] += sm.ktab[time_index(ts_i32 - t4.y)];
-            x[4 * q4 + 2] += sm.ktab[time_index(ts_i32 - t4.z)];
-            x[4 * q4 + 3] += sm.ktab[time_index(ts_i32 - t4.w)];
+            x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
+            x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
+            x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
+            x[4 * q4 + 3] += ktab[time_index(ts_i32 - t4.w)];
           }
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            x[r] += tw[time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
+            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
       }
       const float fN = (float)P.N;
@@ -401,29 +486,9 @@ attn_fwd_kernel(KParams P) {
     }
 
     // sum the two key halves, store O (bf16)
-    lds_barrier();
-    if (wj == 1) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          sm.red[wi][c_row(r, g) * D + 32 * db + l32] = oacc[db][r];
-    }
-    lds_barrier();
-    if (wj == 0) {
-      u16 *o = P.out0 + ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int il = 32 * wi + c_row(r, g);
-          const float val = oacc[db][r] + sm.red[wi][c_row(r, g) * D + 32 * db + l32];
-          if (il < q_valid) {
-            __bf16 bv = (__bf16)val;
-            o[il * row_stride + 32 * db + l32] = __builtin_bit_cast(u16, bv);
-          }
-        }
-    }
+    sum_store_tile<D>(&sm.red[0][0], oacc, wj == 0, wi, g, l32, tid,
+                      P.out0 + ((si.start + (int64_t)qt * TILE) * P.H + h) * D,
+                      row_stride, q_valid);
   }
 }
 
@@ -432,11 +497,12 @@ template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_dq_kernel(KParams P) {
   __shared__ StreamSmem<D> sm;
-  extern __shared__ float tw[];
+  extern __shared__ float dyn[];
   constexpr int ST = D + RM_PAD;
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
   if (tid0 < 2) sm.flag[tid0] = 0;
+  if (TIME) stage_all_heads(P, dyn, tid0);
   int phase = 0;
 
   for (;;) {
@@ -467,13 +533,14 @@ attn_dq_kernel(KParams P) {
     int64_t ts_start = 0, ts_i = 0;
     int32_t ts_i32 = 0;
     bool q_far = false;
+    float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      stage_time_tables<D>(P, sm, tw, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid);
     }
 
     f32x16 acc[D / 32];
@@ -546,15 +613,15 @@ attn_dq_kernel(KParams P) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
             const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
-            x[4 * q4 + 0] += sm.ktab[time_index(ts_i32 - t4.x)];
-            x[4 * q4 + 1] += sm.ktab[time_index(ts_i32 - t4.y)];
-            x[4 * q4 + 2] += sm.ktab[time_index(ts_i32 - t4.z)];
-            x[4 * q4 + 3] += sm.ktab[time_index(ts_i32 - t4.w)];
+            x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
+            x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
+            x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
+            x[4 * q4 + 3] += ktab[time_index(ts_i32 - t4.w)];
           }
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            x[r] += tw[time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
+            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
       }
       float dsv[16];
@@ -581,29 +648,8 @@ attn_dq_kernel(KParams P) {
       }
     }
 
-    lds_barrier();
-    if (wj == 1) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          sm.red[wi][c_row(r, g) * D + 32 * db + l32] = acc[db][r];
-    }
-    lds_barrier();
-    if (wj == 0) {
-      u16 *dq = P.out0 + qoff;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int il = 32 * wi + c_row(r, g);
-          const float val = acc[db][r] + sm.red[wi][c_row(r, g) * D + 32 * db + l32];
-          if (il < q_valid) {
-            __bf16 bv = (__bf16)val;
-            dq[il * row_stride + 32 * db + l32] = __builtin_bit_cast(u16, bv);
-          }
-        }
-    }
+    sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.out0 + qoff,
+                      row_stride, q_valid);
   }
 }
 
@@ -623,7 +669,7 @@ struct DkvSmem {
   // (m & 127): a tile pair touches 127 consecutive diagonals, the next one
   // shifts them by 64, so only completed diagonals leave for global memory
   float dwin[POS ? 2 * TILE : 1];
-  float kacc[KTAB];             // this item's d_time by float-exponent index
+  fix64 kacc[KTAB];             // this item's d_time by float-exponent index
 };
 
 template <int D, bool POS, bool TIME>
@@ -631,16 +677,18 @@ __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_dkv_kernel(KParams P) {
   __shared__ DkvSmem<D, POS> smx;
   StreamSmem<D> &sm = smx.s;
-  extern __shared__ float dyn[];             // [nb] time_w row, then [H][nb] d_time
-  float *tw = dyn;
-  float *tacc = dyn + P.nb;
+  // dynamic LDS: [H][nb] d_time (fixed point), then the time tables
+  extern __shared__ fix64 dyn_k[];
+  fix64 *tacc = dyn_k;
+  float *dyn = (float *)(dyn_k + P.H * P.nb);
   constexpr int ST = D + RM_PAD;
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
 
   if (TIME) {
-    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0f;
-    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0f;
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
+    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0;
+    stage_all_heads(P, dyn, tid0);
   }
   if (tid0 < 2) sm.flag[tid0] = 0;
   if (POS) {
@@ -650,6 +698,12 @@ attn_dkv_kernel(KParams P) {
     for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
   }
   int phase = 0;
+  // A finished d_pos diagonal sum is sent one tile later, right after the
+  // next wait for the prefetched tiles: the wait counter also counts
+  // atomics, so sending it at the end of its own tile would put a full
+  // atomic round trip into every iteration.
+  float *pend_p = nullptr;
+  float pend_v = 0.0f;
 
   for (;;) {
     if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
@@ -679,16 +733,17 @@ attn_dkv_kernel(KParams P) {
     int64_t ts_start = 0, ts_j = 0;
     int32_t ts_j32 = 0;
     bool k_far = false;
+    float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_j = j_loc < k_valid ? P.ts[si.start + (int64_t)kt * TILE + j_loc] : ts_start;
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
-      stage_time_tables<D>(P, sm, tw, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid);
     }
     TimeRun run;                              // fast path: by float-exponent index
-    float *my_t = TIME ? tacc + h * P.nb : nullptr;
+    fix64 *my_t = TIME ? tacc + h * P.nb : nullptr;
 
     f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -711,7 +766,11 @@ attn_dkv_kernel(KParams P) {
       lds_barrier();
       qr.store(sm.t.a, tid);
       dr.store(sm.t.b, tid);
-      if (POS) pos_store<true>(pos_v, sm.pos, tid);
+      if (POS) {
+        pos_store<true>(pos_v, sm.pos, tid);
+        if (pend_p) atomicAdd(pend_p, pend_v);
+        pend_p = nullptr;
+      }
       if (TIME) {
         bool far = k_far;
         if (tid < TILE) {
@@ -773,26 +832,31 @@ attn_dkv_kernel(KParams P) {
             tk[4 * q4 + 3] = time_index(t4.w - ts_j32);
           }
 #pragma unroll
-          for (int r = 0; r < 16; ++r) x[r] += sm.ktab[tk[r]];
+          for (int r = 0; r < 16; ++r) x[r] += ktab[tk[r]];
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             tk[r] = time_bucket(sm.ts64[ib + c_row(r, 0)] - ts_j, P.nb);
-            x[r] += tw[tk[r]];
+            x[r] += ktab[KTAB + tk[r]];
           }
         }
       }
-      const bool diag = (qt == kt);
+      // a = silu(x)/N, dS = dA silu'(x)/N = dA (sg + a' (1 - sg))/N with
+      // a' = x sg.  Query rows past the sequence have dO = 0, hence dA = 0
+      // and dS = 0, and contribute a * 0 to dV: only the diagonal tile
+      // needs a mask (the causal one).
       float av[16], dsv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int i_loc = ib + c_row(r, 0);
-        const bool valid = (i_loc < q_valid) && (!diag || i_loc >= j_loc);
         const float sg = sigmoid_f(x[r]);
-        const float a = x[r] * sg * P.inv_n;
-        const float ds = da[r] * sg * __builtin_fmaf(x[r], 1.0f - sg, 1.0f) * P.inv_n;
-        av[r] = valid ? a : 0.0f;
-        dsv[r] = valid ? ds : 0.0f;
+        const float a1 = x[r] * sg;
+        av[r] = a1 * P.inv_n;
+        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1) * P.inv_n;
+      }
+      if (qt == kt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (ib + c_row(r, 0) < j_loc) { av[r] = 0.0f; dsv[r] = 0.0f; }
       }
       if (POS) {
         // element (i, j) -> shear[i][j - i + 63]; i = ib + c_row(r, 0)
@@ -810,7 +874,7 @@ attn_dkv_kernel(KParams P) {
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (dsv[r] != 0.0f) atomicAdd(&my_t[tk[r]], dsv[r]);
+            if (dsv[r] != 0.0f) atomicAdd(&my_t[tk[r]], to_fixed(dsv[r]));
         }
       }
 
@@ -858,8 +922,10 @@ attn_dkv_kernel(KParams P) {
           const float acc = smx.dwin[slot] + ((v0 + v1) + (v2 + v3));
           if (c >= TILE - 1 || qt + 1 == si.ntiles) {
             smx.dwin[slot] = 0.0f;
-            if (acc != 0.0f && m >= 0 && m < si.len)
-              atomicAdd(&P.dpos_part[(si.start + m) * P.H + h], acc);
+            if (acc != 0.0f && m >= 0 && m < si.len) {
+              pend_p = &P.dpos_part[(si.start + m) * P.H + h];
+              pend_v = acc;
+            }
           } else {
             smx.dwin[slot] = acc;
           }
@@ -873,59 +939,25 @@ attn_dkv_kernel(KParams P) {
     lds_barrier();
     if (TIME) {
       for (int x = tid; x < KTAB; x += THREADS) {
-        const float val = smx.kacc[x];
-        if (val != 0.0f) {
-          smx.kacc[x] = 0.0f;
+        const fix64 val = smx.kacc[x];
+        if (val != 0) {
+          smx.kacc[x] = 0;
           atomicAdd(&my_t[bucket_of_index(x, P.nb)], val);
         }
       }
     }
-    if (wi == 1) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          sm.red[wj][c_row(r, g) * D + 32 * db + l32] = dk[db][r];
-    }
-    lds_barrier();
-    if (wi == 0) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) dk[db][r] += sm.red[wj][c_row(r, g) * D + 32 * db + l32];
-    }
-    lds_barrier();
-    if (wi == 1) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          sm.red[wj][c_row(r, g) * D + 32 * db + l32] = dv[db][r];
-    }
-    lds_barrier();
-    if (wi == 0) {
-      u16 *dko = P.out0 + koff;
-      u16 *dvo = P.out1 + koff;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int jl = 32 * wj + c_row(r, g);
-          const float vv = dv[db][r] + sm.red[wj][c_row(r, g) * D + 32 * db + l32];
-          if (jl < k_valid) {
-            __bf16 bk = (__bf16)dk[db][r], bv = (__bf16)vv;
-            dko[jl * row_stride + 32 * db + l32] = __builtin_bit_cast(u16, bk);
-            dvo[jl * row_stride + 32 * db + l32] = __builtin_bit_cast(u16, bv);
-          }
-        }
-    }
+    sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
+                      row_stride, k_valid);
+    sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
+                      row_stride, k_valid);
   }
+  if (POS && pend_p) atomicAdd(pend_p, pend_v);
   if (TIME) {
     // fold this work-group's histogram into one of DTIME_BINS partials
     lds_barrier();
     float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
     for (int x = tid0; x < P.H * P.nb; x += THREADS)
-      if (tacc[x] != 0.0f) atomicAdd(&part[x], tacc[x]);
+      if (tacc[x] != 0) atomicAdd(&part[x], from_fixed(tacc[x]));
   }
 }
 
@@ -938,6 +970,21 @@ int persistent_grid(K kernel, size_t dyn, int64_t items, int dev) {
     occ = 1;
   const int64_t cap = (int64_t)device_info(dev).num_cu * occ;
   return (int)std::max<int64_t>(1, std::min<int64_t>(cap, items));
+}
+
+// Time tables: one slot of KTAB + nb floats per head when all heads fit in
+// this budget (staged once per work-group), else a single per-item slot.
+constexpr size_t ALL_HEADS_BUDGET = 32 * 1024;
+bool all_heads(const Problem &p) {
+  return p.has_time && sizeof(float) * (size_t)p.H * (KTAB + p.nb) <= ALL_HEADS_BUDGET;
+}
+size_t slots_bytes(const Problem &p) {
+  if (!p.has_time) return 0;
+  return sizeof(float) * (size_t)(all_heads(p) ? p.H : 1) * (KTAB + p.nb);
+}
+size_t q_dyn_bytes(const Problem &p) { return slots_bytes(p); }
+size_t k_dyn_bytes(const Problem &p) {
+  return p.has_time ? slots_bytes(p) + sizeof(unsigned long long) * (size_t)p.nb * p.H : 0;
 }
 
 KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
@@ -957,6 +1004,7 @@ KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
   P.N = a.p.N;
   P.nb = a.p.has_time ? a.p.nb : 0;
   P.inv_n = 1.0f / (float)a.p.N;
+  P.all_heads = all_heads(a.p) ? 1 : 0;
   return P;
 }
 
@@ -981,10 +1029,6 @@ int current_dev() {
   return dev;
 }
 
-size_t q_dyn_bytes(const Problem &p) { return p.has_time ? sizeof(float) * p.nb : 0; }
-size_t k_dyn_bytes(const Problem &p) {
-  return p.has_time ? sizeof(float) * (size_t)p.nb * (p.H + 1) : 0;
-}
 
 }  // namespace
 
