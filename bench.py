@@ -35,7 +35,7 @@ PEAK_FP32_TFLOPS = 157.3           # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # flop per byte
 
-KERNEL_SOURCES = ["device.h", "internal.h", "sched.hip", "attn_bf16.hip",
+KERNEL_SOURCES = ["device.h", "internal.h", "sched_impl.h", "sched.hip", "attn_bf16.hip",
                   "attn_f32.hip", "norm.hip", "api.cpp"]
 
 

@@ -324,16 +324,17 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
   float *d_pos = p.has_pos ? io->d_pos_w : nullptr;
   float *d_time = p.has_time ? io->d_time_w : nullptr;
   hipError_t e;
-  {
+  if (p.T > 0) {
+    // the LayerNorm backward launch also builds the work lists
+    prof::Scope ps("ln_bwd", s);
+    e = launch_ln_bwd_sched(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
+                            ws + L.dO, L.dpos_part ? (float *)(ws + L.dpos_part) : nullptr,
+                            seq_offsets, ws, L, s);
+    if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
+  } else {
     prof::Scope ps("schedule", s);
     e = launch_schedule(seq_offsets, p, ws, L, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "schedule launch");
-  if (p.T > 0) {
-    prof::Scope ps("ln_bwd", s);
-    e = launch_ln_bwd(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
-                      ws + L.dO, L.dpos_part ? (float *)(ws + L.dpos_part) : nullptr, s);
-    if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
+    if (e != hipSuccess) return hip_fail(e, "schedule launch");
   }
   if (p.dtype == HSTU_BF16) {
     if (p.T > 0) {

@@ -122,9 +122,13 @@ hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
 
 hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
                          void *y, float *mean, float *rstd, hipStream_t s);
-hipError_t launch_ln_bwd(const Problem &p, const void *dy, const void *u,
-                         const void *o, const float *mean, const float *rstd,
-                         void *du, void *dO, float *dpos_part, hipStream_t s);
+// LayerNorm backward with the scheduler's work-group appended: builds the
+// backward's lists (as launch_schedule) in the same launch.
+hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
+                               const void *o, const float *mean, const float *rstd,
+                               void *du, void *dO, float *dpos_part,
+                               const int64_t *seq_offsets, void *ws, const Layout &L,
+                               hipStream_t s);
 hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                                   float *d_time, hipStream_t s);
 

@@ -13,6 +13,7 @@
 
 #include "internal.h"
 #include "device.h"
+#include "sched_impl.h"
 
 namespace hstu {
 
@@ -103,15 +104,23 @@ ln_fwd_kernel(const T *__restrict__ o, const T *__restrict__ u,
   }
 }
 
+// With `sched` set, the launch's first work-group (dispatched first, so its
+// serial phases overlap the rest) builds the backward's work lists
+// (sched_impl.h) while the others normalise.
 template <typename T>
 __global__ void __launch_bounds__(LN_THREADS)
 ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
               const T *__restrict__ o, const float *__restrict__ mean,
               const float *__restrict__ rstd, T *__restrict__ du,
               T *__restrict__ dO, float *__restrict__ dpos_part, int H,
-              int64_t T_tokens, int F) {
+              int64_t T_tokens, int F, SchedArgs sa, int sched) {
+  if (sched && blockIdx.x == 0) {
+    __shared__ SchedSmem ssm;
+    build_schedule<LN_THREADS>(sa, ssm, threadIdx.x);
+    return;
+  }
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
+  const int64_t r = (int64_t)(blockIdx.x - sched) * LN_WAVES + (threadIdx.x >> 6);
   if (r >= T_tokens) return;
   const float mu = mean[r], rs = rstd[r];
   const int64_t base = r * F;
@@ -159,7 +168,7 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 //     columns; waves stride over the bins.
 // Summation order is fixed, so the result is deterministic given the
 // partials.
-constexpr int FIN_THREADS = 512;
+constexpr int FIN_THREADS = 1024;
 constexpr int FIN_WAVES = FIN_THREADS / 64;
 
 __global__ void __launch_bounds__(FIN_THREADS)
@@ -176,10 +185,23 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
     const int h = blockIdx.x / chunks;
     const int m = (blockIdx.x % chunks) * 64 + lane;
     if (m < N) {
-      for (int b = wv; b < B; b += FIN_WAVES) {
+      // four sequences per step, loads issued together (no dependent chain)
+      float a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      int b = wv;
+      for (; b + 3 * FIN_WAVES < B; b += 4 * FIN_WAVES) {
+        const SeqInfo s0 = info[b], s1 = info[b + FIN_WAVES];
+        const SeqInfo s2 = info[b + 2 * FIN_WAVES], s3 = info[b + 3 * FIN_WAVES];
+        const float v0 = s0.len > m ? pos_part[(s0.start + m) * H + h] : 0.0f;
+        const float v1 = s1.len > m ? pos_part[(s1.start + m) * H + h] : 0.0f;
+        const float v2 = s2.len > m ? pos_part[(s2.start + m) * H + h] : 0.0f;
+        const float v3 = s3.len > m ? pos_part[(s3.start + m) * H + h] : 0.0f;
+        acc += v0; a1 += v1; a2 += v2; a3 += v3;
+      }
+      for (; b < B; b += FIN_WAVES) {
         const SeqInfo si = info[b];
         if (si.len > m) acc += pos_part[(si.start + m) * H + h];
       }
+      acc += (a1 + a2) + a3;
     }
     red[wv][lane] = acc;
     __syncthreads();
@@ -219,19 +241,22 @@ hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
   return hipGetLastError();
 }
 
-hipError_t launch_ln_bwd(const Problem &p, const void *dy, const void *u,
-                         const void *o, const float *mean, const float *rstd,
-                         void *du, void *dO, float *dpos_part, hipStream_t s) {
+hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
+                               const void *o, const float *mean, const float *rstd,
+                               void *du, void *dO, float *dpos_part,
+                               const int64_t *seq_offsets, void *ws, const Layout &L,
+                               hipStream_t s) {
   const int F = p.H * p.d;
-  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES));
+  const SchedArgs sa = sched_args(seq_offsets, p, ws, L);
+  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES) + 1);
   if (p.dtype == HSTU_BF16)
     hipLaunchKernelGGL(ln_bwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
                        (const u16 *)dy, (const u16 *)u, (const u16 *)o, mean, rstd,
-                       (u16 *)du, (u16 *)dO, dpos_part, p.H, p.T, F);
+                       (u16 *)du, (u16 *)dO, dpos_part, p.H, p.T, F, sa, 1);
   else
     hipLaunchKernelGGL(ln_bwd_kernel<float>, grid, dim3(LN_THREADS), 0, s,
                        (const float *)dy, (const float *)u, (const float *)o, mean, rstd,
-                       (float *)du, (float *)dO, dpos_part, p.H, p.T, F);
+                       (float *)du, (float *)dO, dpos_part, p.H, p.T, F, sa, 1);
   return hipGetLastError();
 }
 
