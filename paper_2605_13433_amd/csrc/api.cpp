@@ -180,9 +180,10 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   L.seqinfo = take(sizeof(SeqInfo) * (size_t)std::max(p.B, 1));
   L.list_q = take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1));
   L.list_k = for_bwd ? take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
+  L.list_b = for_bwd ? take(2 * sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
   L.dO = for_bwd ? take(elem * (size_t)p.T * p.H * p.d) : 0;
   const bool bf16_bwd = for_bwd && p.dtype == HSTU_BF16;
-  L.dkv_grid = bf16_bwd ? attn_dkv_grid(p, dev) : 0;
+  L.bwd_grid = bf16_bwd ? attn_bwd_grid(p, dev) : 0;
   L.dpos_part = (bf16_bwd && p.has_pos) ? take(sizeof(float) * (size_t)p.T * p.H) : 0;
   L.dtime_part = (bf16_bwd && p.has_time)
                      ? take(sizeof(float) * (size_t)DTIME_BINS * p.H * p.nb)
@@ -337,16 +338,11 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
     if (e != hipSuccess) return hip_fail(e, "schedule launch");
   }
   if (p.dtype == HSTU_BF16) {
-    if (p.T > 0) {
-      prof::Scope ps("attn_dq", s);
-      e = launch_attn_dq_bf16(a, ws + L.dO, io->dq, s);
-      if (e != hipSuccess) return hip_fail(e, "attention dQ launch");
-    }
     {
-      prof::Scope ps("attn_dkv", s);
-      e = launch_attn_dkv_bf16(a, ws + L.dO, io->dk, io->dv, s);
+      prof::Scope ps("attn_bwd", s);
+      e = launch_attn_bwd_bf16(a, ws + L.dO, io->dq, io->dk, io->dv, s);
     }
-    if (e != hipSuccess) return hip_fail(e, "attention dK/dV launch");
+    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
     {
       prof::Scope ps("finalize_tables", s);
       e = launch_finalize_tables(a, d_pos, d_time, s);

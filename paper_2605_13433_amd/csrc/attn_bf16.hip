@@ -2,15 +2,16 @@
 // QKV with the relative position and relative time biases fused into the
 // attention kernel, no padding and no dense<->jagged conversion).
 //
-// Three persistent kernels pop (sequence, 64-row tile, head) items from the
+// Two persistent kernels pop (sequence, 64-row tile, head) items from the
 // scheduler's longest-first lists:
 //
 //   attn_fwd   q-stationary: O_i = sum_{j<=i} silu(s_ij)/N v_j
-//   attn_dq    q-stationary: dQ_i = sum_{j<=i} dS_ij k_j
-//   attn_dkv   k-stationary: dV_j = sum_{i>=j} a_ij dO_i,
-//                            dK_j = sum_{i>=j} dS_ij q_i, plus the table
-//                            gradients (per-sequence diagonal partials for
-//                            d_pos, binned per-work-group histograms for d_time)
+//   attn_bwd   one launch over two item kinds:
+//              dQ items, q-stationary: dQ_i = sum_{j<=i} dS_ij k_j
+//              dK/dV items, k-stationary: dV_j = sum_{i>=j} a_ij dO_i,
+//                dK_j = sum_{i>=j} dS_ij q_i, plus the table gradients
+//                (per-sequence diagonal partials for d_pos, binned
+//                per-work-group histograms for d_time)
 //
 // with s_ij = <q_i,k_j> + pos_w[h, j-i+N-1] + time_w[h, bucket(ts_i-ts_j)],
 // dS_ij = <dO_i, v_j> silu'(s_ij) / N, and the causal mask applied after the
@@ -63,6 +64,7 @@ struct KParams {
   const SeqInfo *info;
   const WorkEntry *list;
   u16 *out0, *out1;
+  u16 *dq_out;
   float *dpos_part, *dtime_part;
   int32_t H, N, nb;
   float inv_n;
@@ -493,23 +495,13 @@ attn_fwd_kernel(KParams P) {
 }
 
 // --------------------------------------------------------------------- dQ
+// One q-stationary item: dQ_i = sum_{j<=i} dS_ij k_j for a 64-row query tile
+// of one head, recomputing S and dA = dO V^T tile by tile.
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
-attn_dq_kernel(KParams P) {
-  __shared__ StreamSmem<D> sm;
-  extern __shared__ float dyn[];
+__device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, float *dyn,
+                                        const int tid0, const WorkEntry e, const int h,
+                                        int &phase) {
   constexpr int ST = D + RM_PAD;
-  const int tid0 = threadIdx.x;
-  const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  if (tid0 < 2) sm.flag[tid0] = 0;
-  if (TIME) stage_all_heads(P, dyn, tid0);
-  int phase = 0;
-
-  for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
     int tid = tid0;
     asm volatile("" : "+v"(tid));
     int row_stride = P.H * D;
@@ -518,8 +510,6 @@ attn_dq_kernel(KParams P) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wi = w & 1, wj = w >> 1;
 
-    const WorkEntry e = P.list[item / P.H];
-    const int h = item % P.H;
     const SeqInfo si = P.info[e.seq];
     const int qt = e.tile;
     const int q_valid = si.len - qt * TILE;
@@ -648,9 +638,8 @@ attn_dq_kernel(KParams P) {
       }
     }
 
-    sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.out0 + qoff,
+    sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
                       row_stride, q_valid);
-  }
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -672,44 +661,16 @@ struct DkvSmem {
   fix64 kacc[KTAB];             // this item's d_time by float-exponent index
 };
 
+// One k-stationary item: dV_j, dK_j for a 64-row key tile of one head over
+// its query tiles, with the table gradients (d_pos through the sheared tile
+// and the rolling diagonal window, d_time through per-lane index runs).
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
-attn_dkv_kernel(KParams P) {
-  __shared__ DkvSmem<D, POS> smx;
-  StreamSmem<D> &sm = smx.s;
-  // dynamic LDS: [H][nb] d_time (fixed point), then the time tables
-  extern __shared__ fix64 dyn_k[];
-  fix64 *tacc = dyn_k;
-  float *dyn = (float *)(dyn_k + P.H * P.nb);
+__device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx, float *dyn,
+                                         fix64 *tacc, const int tid0, const WorkEntry e,
+                                         const int h, int &phase, float *&pend_p,
+                                         float &pend_v) {
   constexpr int ST = D + RM_PAD;
-  const int tid0 = threadIdx.x;
-  const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-
-  if (TIME) {
-    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
-    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0;
-    stage_all_heads(P, dyn, tid0);
-  }
-  if (tid0 < 2) sm.flag[tid0] = 0;
-  if (POS) {
-    if (tid0 < 2 * TILE) smx.dwin[tid0] = 0.0f;
-    // positions (i, j - i + 63) with j outside the tile are never written
-    // again, so zero once: the column sums below read every row
-    for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
-  }
-  int phase = 0;
-  // A finished d_pos diagonal sum is sent one tile later, right after the
-  // next wait for the prefetched tiles: the wait counter also counts
-  // atomics, so sending it at the end of its own tile would put a full
-  // atomic round trip into every iteration.
-  float *pend_p = nullptr;
-  float pend_v = 0.0f;
-
-  for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
+  StreamSmem<D> &sm = smx.s;
     int tid = tid0;
     asm volatile("" : "+v"(tid));
     int row_stride = P.H * D;
@@ -718,8 +679,6 @@ attn_dkv_kernel(KParams P) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wj = w & 1, wi = w >> 1;        // key half (stationary), query half
 
-    const WorkEntry e = P.list[item / P.H];
-    const int h = item % P.H;
     const SeqInfo si = P.info[e.seq];
     const int kt = e.tile;
     const int k_valid = si.len - kt * TILE;
@@ -950,6 +909,57 @@ attn_dkv_kernel(KParams P) {
                       row_stride, k_valid);
     sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
                       row_stride, k_valid);
+}
+
+// Backward: one persistent launch over the combined list, whose entries are
+// dK/dV items (k-stationary) and dQ items (flagged, q-stationary) in one
+// longest-first order, so the two item kinds overlap instead of running as
+// two launches back to back.
+template <int D, bool POS, bool TIME>
+__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
+attn_bwd_kernel(KParams P) {
+  __shared__ DkvSmem<D, POS> smx;
+  StreamSmem<D> &sm = smx.s;
+  // dynamic LDS: [H][nb] d_time (fixed point), then the time tables
+  extern __shared__ fix64 dyn_k[];
+  fix64 *tacc = dyn_k;
+  float *dyn = (float *)(dyn_k + P.H * P.nb);
+  const int tid0 = threadIdx.x;
+  const int n_items = 2 * P.ctrl[CTRL_N_ENTRIES] * P.H;
+
+  if (TIME) {
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
+    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0;
+    stage_all_heads(P, dyn, tid0);
+  }
+  if (tid0 < 2) sm.flag[tid0] = 0;
+  if (POS) {
+    if (tid0 < 2 * TILE) smx.dwin[tid0] = 0.0f;
+    // positions (i, j - i + 63) with j outside the tile are never written
+    // again, so zero once: the column sums below read every row
+    for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
+  }
+  int phase = 0;
+  // A finished d_pos diagonal sum is sent one tile later, right after the
+  // next wait for the prefetched tiles: the wait counter also counts
+  // atomics, so sending it at the end of its own tile would put a full
+  // atomic round trip into every iteration.
+  float *pend_p = nullptr;
+  float pend_v = 0.0f;
+
+  for (;;) {
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
+    lds_barrier();
+    const int item = sm.item;
+    if (item >= n_items) break;
+    WorkEntry e = P.list[item / P.H];
+    const int h = item % P.H;
+    if (e.tile & BWD_DQ_FLAG) {
+      e.tile &= ~BWD_DQ_FLAG;
+      dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase);
+    } else {
+      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v);
+    }
   }
   if (POS && pend_p) atomicAdd(pend_p, pend_v);
   if (TIME) {
@@ -1039,17 +1049,10 @@ int attn_fwd_grid(const Problem &p, int dev) {
   return grid;
 }
 
-int attn_dq_grid(const Problem &p, int dev) {
+int attn_bwd_grid(const Problem &p, int dev) {
   int grid = 1;
-  HSTU_DISPATCH(attn_dq_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
-  return grid;
-}
-
-int attn_dkv_grid(const Problem &p, int dev) {
-  int grid = 1;
-  HSTU_DISPATCH(attn_dkv_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, k_dyn_bytes(p), p.max_entries * p.H, dev));
+  HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
+                grid = persistent_grid(kfn, k_dyn_bytes(p), 2 * p.max_entries * p.H, dev));
   return grid;
 }
 
@@ -1065,33 +1068,20 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_dq_bf16(const AttnArgs &a, const void *dO, void *dq,
-                               hipStream_t s) {
-  const char *ws = (const char *)a.ws;
-  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DQ,
-                          (const WorkEntry *)(ws + a.L.list_q));
-  P.dO = (const u16 *)dO;
-  P.out0 = (u16 *)dq;
-  const Problem &p = a.p;
-  const int grid = attn_dq_grid(p, current_dev());
-  HSTU_DISPATCH(attn_dq_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), q_dyn_bytes(p), s, P));
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_dkv_bf16(const AttnArgs &a, const void *dO, void *dk,
+hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
                                 void *dv, hipStream_t s) {
   const char *ws = (const char *)a.ws;
-  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DKV,
-                          (const WorkEntry *)(ws + a.L.list_k));
+  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_BWD,
+                          (const WorkEntry *)(ws + a.L.list_b));
   P.dO = (const u16 *)dO;
   P.out0 = (u16 *)dk;
   P.out1 = (u16 *)dv;
+  P.dq_out = (u16 *)dq;
   P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
   P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
   const Problem &p = a.p;
-  const int grid = a.L.dkv_grid;
-  HSTU_DISPATCH(attn_dkv_kernel, p.d, p.has_pos, p.has_time,
+  const int grid = a.L.bwd_grid;
+  HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
                 hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), k_dyn_bytes(p), s, P));
   return hipGetLastError();
 }

@@ -24,7 +24,8 @@ enum CtrlSlot {
   CTRL_N_ENTRIES = 0,   // (sequence, tile) entries in each work list
   CTRL_POP_FWD = 1,     // pop counter of the attention forward kernel
   CTRL_POP_DQ = 2,      // pop counter of the dQ kernel
-  CTRL_POP_DKV = 3,     // pop counter of the dK/dV kernel
+  CTRL_POP_DKV = 3,     // pop counter of the fp32 dK/dV pass
+  CTRL_POP_BWD = 4,     // pop counter of the bf16 backward kernel
   CTRL_WORDS = 64
 };
 
@@ -42,6 +43,10 @@ struct WorkEntry {
   int32_t tile;
 };
 
+// In the combined backward list, dQ entries carry this bit in `tile`
+// (dK/dV entries do not).
+constexpr int32_t BWD_DQ_FLAG = 1 << 30;
+
 struct Problem {
   int32_t B, N, H, d;
   int64_t T;
@@ -54,8 +59,8 @@ struct Problem {
 // Workspace carve-up; offsets in bytes from the workspace base, each region
 // 256-byte aligned.  Regions with size 0 are absent.
 struct Layout {
-  size_t ctrl, seqinfo, list_q, list_k, dO, dpos_part, dtime_part, total;
-  int dkv_grid;          // persistent grid of the dK/dV kernel (WG count)
+  size_t ctrl, seqinfo, list_q, list_k, list_b, dO, dpos_part, dtime_part, total;
+  int bwd_grid;          // persistent grid of the bf16 backward kernel (WG count)
 };
 
 // ---- host helpers shared by the C-ABI translation units ----
@@ -110,9 +115,8 @@ struct AttnArgs {
 };
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s);
-hipError_t launch_attn_dq_bf16(const AttnArgs &a, const void *dO, void *dq,
-                               hipStream_t s);
-hipError_t launch_attn_dkv_bf16(const AttnArgs &a, const void *dO, void *dk,
+// dQ, dK, dV and the table-gradient partials in one launch.
+hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
                                 void *dv, hipStream_t s);
 
 hipError_t launch_attn_fwd_f32(const AttnArgs &a, void *o, hipStream_t s);
@@ -144,7 +148,6 @@ hipError_t launch_zero(void *p, size_t bytes, int dev, hipStream_t s);
 
 // Persistent-grid sizes (work-groups) of the bf16 attention kernels.
 int attn_fwd_grid(const Problem &p, int dev);
-int attn_dq_grid(const Problem &p, int dev);
-int attn_dkv_grid(const Problem &p, int dev);
+int attn_bwd_grid(const Problem &p, int dev);
 
 }  // namespace hstu

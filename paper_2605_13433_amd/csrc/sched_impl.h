@@ -11,9 +11,11 @@
 //
 //   * q-list: entries (b, qt) for every 64-row query tile of every sequence,
 //     cost qt+1 k-tiles (causal: only kt <= qt is visited), sorted by cost
-//     descending.  Consumed by the forward and the dQ kernels.
+//     descending.  Consumed by the forward kernels and the fp32 dQ pass.
 //   * k-list: entries (b, kt), cost ntiles_b - kt q-tiles, same order rule.
-//     Consumed by the dK/dV kernel.
+//     Consumed by the fp32 dK/dV pass.
+//   * combined backward list: both kinds merged bin by bin (dQ entries
+//     flagged), consumed by the bf16 backward kernel.
 //
 // Built on the device from seq_offsets (no host round trip) by one
 // work-group: a histogram of tile counts, a descending exclusive scan of the
@@ -33,6 +35,7 @@ struct SchedSmem {
   int32_t start[SCHED_MAX_BINS];      // first slot of cost bin c
   int32_t fill_q[SCHED_MAX_BINS];
   int32_t fill_k[SCHED_MAX_BINS];
+  int32_t ge[SCHED_MAX_BINS];         // # sequences with ntiles >= c
   int32_t total;
 };
 
@@ -42,7 +45,7 @@ struct SchedArgs {
   int64_t T;
   int32_t *ctrl;
   SeqInfo *info;
-  WorkEntry *list_q, *list_k;
+  WorkEntry *list_q, *list_k, *list_b;
   int32_t nbins, cap;
   float *zero_out;
   int32_t n_zero;
@@ -86,6 +89,7 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     for (int c = a.nbins - 1; c >= 1; --c) {
       ge += sm.count_ge[c];        // sequences with ntiles >= c
       sm.start[c] = run;
+      sm.ge[c] = ge;
       run += ge;
     }
     // Valid offsets never exceed the list capacity; overlapping (invalid)
@@ -95,6 +99,7 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     a.ctrl[CTRL_POP_FWD] = 0;
     a.ctrl[CTRL_POP_DQ] = 0;
     a.ctrl[CTRL_POP_DKV] = 0;
+    a.ctrl[CTRL_POP_BWD] = 0;
   }
   __syncthreads();
 
@@ -107,6 +112,14 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
       const int sk = sm.start[ck] + atomicAdd(&sm.fill_k[ck], 1);
       if (sq < a.cap) a.list_q[sq] = WorkEntry{b, t};
       if (a.list_k && sk < a.cap) a.list_k[sk] = WorkEntry{b, t};
+      if (a.list_b) {
+        // combined backward list: bin c spans 2 ge[c] slots from 2 start[c],
+        // dK/dV entries first (the heavier item of equal cost), then dQ ones
+        const int bk = sk + sm.start[ck];
+        const int bq = sq + sm.start[cq] + sm.ge[cq];
+        if (bk < 2 * a.cap) a.list_b[bk] = WorkEntry{b, t};
+        if (bq < 2 * a.cap) a.list_b[bq] = WorkEntry{b, t | BWD_DQ_FLAG};
+      }
     }
   }
 }
@@ -123,6 +136,7 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.info = (SeqInfo *)(base + L.seqinfo);
   a.list_q = (WorkEntry *)(base + L.list_q);
   a.list_k = L.list_k ? (WorkEntry *)(base + L.list_k) : nullptr;
+  a.list_b = L.list_b ? (WorkEntry *)(base + L.list_b) : nullptr;
   a.nbins = (int)((p.N + TILE - 1) / TILE) + 2;
   a.cap = (int32_t)p.max_entries;
   a.zero_out = L.dtime_part ? (float *)(base + L.dtime_part) : nullptr;
