@@ -656,8 +656,10 @@ struct DkvSmem {
   float shear[POS ? TILE * SHEAR_STRIDE : 1];
   // d_pos of the current item by diagonal m = i - j, rolling over 128 slots
   // (m & 127): a tile pair touches 127 consecutive diagonals, the next one
-  // shifts them by 64, so only completed diagonals leave for global memory
-  float dwin[POS ? 2 * TILE : 1];
+  // shifts them by 64, so only completed diagonals leave for global memory.
+  // Two windows: the upper and lower 32 rows of the tile are summed by
+  // different threads, each keeping (and flushing) its own window.
+  float dwin[POS ? 2 * 2 * TILE : 1];
   fix64 kacc[KTAB];             // this item's d_time by float-exponent index
 };
 
@@ -829,7 +831,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         if (!slow) {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (dsv[r] != 0.0f) run.add(smx.kacc, tk[r], dsv[r]);
+            run.add(smx.kacc, tk[r], dsv[r]);
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
@@ -859,25 +861,25 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
       if (POS) {
         // column c of the sheared tile is diagonal m = (qt-kt)*64 - (c-63);
-        // sum its rows (independent loads; rows outside the tile hold 0),
-        // add it to the
-        // rolling window, and send diagonals no later tile touches
-        // (c >= 63, or every one on the item's last tile) to the sequence's
-        // d_pos partial
+        // thread (c, half) sums rows 32 half .. 32 half + 31 of it
+        // (independent loads; rows outside the tile hold 0), adds that to
+        // its half's rolling window, and sends diagonals no later tile
+        // touches (c >= 63, or every one on the item's last tile) to the
+        // sequence's d_pos partial
         lds_barrier();
-        const int c = tid;
+        const int c = tid & (2 * TILE - 1), half = tid >> 7;
         if (c < 2 * TILE - 1) {
           float v0 = 0.0f, v1 = 0.0f, v2 = 0.0f, v3 = 0.0f;
 #pragma unroll
-          for (int i = 0; i < TILE; i += 4) {
-            const float *col = smx.shear + i * SHEAR_STRIDE + c;
+          for (int i = 0; i < TILE / 2; i += 4) {
+            const float *col = smx.shear + (32 * half + i) * SHEAR_STRIDE + c;
             v0 += col[0];
             v1 += col[SHEAR_STRIDE];
             v2 += col[2 * SHEAR_STRIDE];
             v3 += col[3 * SHEAR_STRIDE];
           }
           const int m = (qt - kt) * TILE - (c - (TILE - 1));
-          const int slot = m & (2 * TILE - 1);
+          const int slot = half * 2 * TILE + (m & (2 * TILE - 1));
           const float acc = smx.dwin[slot] + ((v0 + v1) + (v2 + v3));
           if (c >= TILE - 1 || qt + 1 == si.ntiles) {
             smx.dwin[slot] = 0.0f;
@@ -934,7 +936,7 @@ attn_bwd_kernel(KParams P) {
   }
   if (tid0 < 2) sm.flag[tid0] = 0;
   if (POS) {
-    if (tid0 < 2 * TILE) smx.dwin[tid0] = 0.0f;
+    smx.dwin[tid0] = 0.0f;   // 4 TILE = THREADS slots
     // positions (i, j - i + 63) with j outside the tile are never written
     // again, so zero once: the column sums below read every row
     for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
