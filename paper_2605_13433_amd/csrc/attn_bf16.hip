@@ -327,16 +327,91 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
   }
 }
 
+// ------------------------------------------------- swizzled DMA-fed tiles
+// A 64-row tile of one head in LDS without padding: 16-byte chunk c of row r
+// sits at chunk position c ^ (r & 7) of that row, so the row-wise reads (32
+// lanes on 32 consecutive rows, one chunk each) and the transpose reads spread
+// over all banks.  Tiles are filled straight from global memory by the gfx950
+// global-to-LDS loads (each lane's 16 bytes land at the instruction's LDS base
+// + 16 * lane), so no registers or LDS-store instructions stage them.
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int D>
+__device__ __forceinline__ int swz(int r, int c) {
+  return r * D + 8 * (c ^ (r & 7));
+}
+
+// Issue the loads of a 64 x D tile (rows of `row_stride` elements from
+// `base`) into `lds`; wave w covers 1/4 of it.  Rows at or beyond `valid`
+// (>= 1) repeat row valid-1: finite data that the caller always masks out.
+template <int D>
+__device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid, int row_stride,
+                                         u16 *lds, int w, int lane) {
+  constexpr int CPR = D / 8;                       // 16-byte chunks per row
+  constexpr int IPW = TILE * CPR / 64 / 4;         // load instructions per wave
+#pragma unroll
+  for (int x = 0; x < IPW; ++x) {
+    const int pos = (w * IPW + x) * 64 + lane;     // chunk position in LDS
+    const int r = pos / CPR;
+    const int c = (pos % CPR) ^ (r & 7);
+    const int rr = r < valid ? r : valid - 1;
+    __builtin_amdgcn_global_load_lds((const void *)(base + rr * row_stride + 8 * c),
+                                     (lds_void *)(lds + (w * IPW + x) * 64 * 8), 16, 0, 0);
+  }
+}
+
+// Wait for this wave's outstanding global loads, the LDS-filling ones
+// included (they count as vector memory operations, not LDS operations).
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
+template <int D>
+__device__ __forceinline__ bf16x8 sread_rm(const u16 *lds, int row, int col) {
+  return *(const bf16x8 *)(lds + swz<D>(row, col >> 3));
+}
+
+// As read_tr, on a swizzled tile.
+template <int D>
+__device__ __forceinline__ bf16x8 sread_tr(const u16 *lds, int krow, int ncol, int lane) {
+  const int c = lane & 15;
+  const int row = krow + (c >> 2);
+  const int col = ncol + ((lane >> 4) & 1) * 16 + 4 * (c & 3);
+  const u16 *p0 = lds + swz<D>(row, col >> 3) + (col & 7);
+  const u16 *p1 = lds + swz<D>(row + 8, col >> 3) + (col & 7);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p0);
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p1);
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  const v8i16 x = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, x);
+}
+
+// Forward shared memory: two K/V buffers (tile kt computes from one while
+// tile kt+1 streams into the other), per-parity bias slices, a three-slot
+// "far timestamp" flag.  The cross-wave output sum reuses the tile buffers.
+template <int D>
+struct FwdSmem {
+  union {
+    u16 tile[2][2][TILE * D];            // [buffer][K, V]
+    float red[TILE * D];
+  };
+  alignas(16) float pos[2][4 * POS_COPY];
+  alignas(16) int32_t ts32[2][TILE];
+  int64_t ts64[2][TILE];
+  int flag[3];
+  int item;
+};
+
 // ---------------------------------------------------------------- forward
+// One work-group barrier per key tile: the barrier of tile kt publishes its
+// DMA-filled buffers and bias slices, and proves every wave is done with
+// tile kt-1, whose buffer then takes tile kt+1.
 template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, 2)
 attn_fwd_kernel(KParams P) {
-  __shared__ StreamSmem<D> sm;
+  __shared__ FwdSmem<D> sm;
   extern __shared__ float dyn[];              // time tables (see item_time_slot)
-  constexpr int ST = D + RM_PAD;
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  if (tid0 < 2) sm.flag[tid0] = 0;
+  if (tid0 < 3) sm.flag[tid0] = 0;
   if (TIME) stage_all_heads(P, dyn, tid0);
   int phase = 0;
 
@@ -363,6 +438,12 @@ attn_fwd_kernel(KParams P) {
     const int q_valid = si.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
     const u16 *qbase = P.q + ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
+    const u16 *kbase = P.k + (si.start * P.H + h) * D;
+    const u16 *vbase = P.v + (si.start * P.H + h) * D;
+
+    // key tile 0 starts streaming before anything else
+    dma_tile<D>(kbase, si.len, row_stride, sm.tile[phase & 1][0], w, lane);
+    dma_tile<D>(vbase, si.len, row_stride, sm.tile[phase & 1][1], w, lane);
 
     bf16x8 qreg[D / 16];
     load_stationary<D>(qbase, i_loc, q_valid, row_stride, g, qreg);
@@ -386,42 +467,38 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
 
-    TileRegs<D> kr, vr;
     int64_t ts_k = 0;
     float pos_v = 0.0f;
-    {
-      kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
-      vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
-      if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
-      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
-    }
+    if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
+    if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
 
     for (int kt = 0; kt <= qt; ++kt, ++phase) {
-      lds_barrier();
-      kr.store(sm.t.a, tid);
-      vr.store(sm.t.b, tid);
-      if (POS) pos_store<false>(pos_v, sm.pos, tid);
+      const int pb = phase & 1, fs = phase % 3;
+      if (POS) pos_store<false>(pos_v, sm.pos[pb], tid);
       if (TIME) {
         bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
-          sm.ts32[tid] = (int32_t)rel;
-          sm.ts64[tid] = ts_k;
+          sm.ts32[pb][tid] = (int32_t)rel;
+          sm.ts64[pb][tid] = ts_k;
           far |= rel >= NEAR || rel <= -NEAR;
         }
-        if (far) sm.flag[phase & 1] = 1;
+        if (far) sm.flag[fs] = 1;
       }
+      wait_vm();
       lds_barrier();
-      const bool slow = TIME && sm.flag[phase & 1] != 0;
-      if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
-      if (kt < qt) {       // prefetch the next key tile while this one computes
+      const bool slow = TIME && sm.flag[fs] != 0;
+      if (TIME && tid == 0) sm.flag[(phase + 2) % 3] = 0;
+      if (kt < qt) {       // stream the next key tile into the other buffer
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
-        kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
-        vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
+        dma_tile<D>(P.k + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][0], w, lane);
+        dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       }
+      const u16 *kt_lds = sm.tile[pb][0];
+      const u16 *vt_lds = sm.tile[pb][1];
 
       // S^T quadrant [32 keys x 32 queries] = K_wj Q_wi^T
       f32x16 s;
@@ -429,7 +506,7 @@ attn_fwd_kernel(KParams P) {
       for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks)
-        s = mfma32(read_rm(sm.t.a, ST, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
+        s = mfma32(sread_rm<D>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
 
       // bias: this lane's keys sit at 32 wj + 4 g + 8 q4 + c
       float x[16];
@@ -437,19 +514,19 @@ attn_fwd_kernel(KParams P) {
       for (int r = 0; r < 16; ++r) x[r] = s[r];
       const int kb = 32 * wj + 4 * g;
       if (POS) {
-        const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
+        const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
-          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+          const float4 pbv = *(const float4 *)(pl + 8 * q4);
+          x[4 * q4 + 0] += pbv.x; x[4 * q4 + 1] += pbv.y;
+          x[4 * q4 + 2] += pbv.z; x[4 * q4 + 3] += pbv.w;
         }
       }
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
+            const int4 t4 = *(const int4 *)(sm.ts32[pb] + kb + 8 * q4);
             x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
             x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
             x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
@@ -458,13 +535,16 @@ attn_fwd_kernel(KParams P) {
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
+            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[pb][kb + c_row(r, 0)], P.nb)];
         }
       }
       const float fN = (float)P.N;
       float av[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) av[r] = silu_over_n(x[r], fN);
+      // the diagonal tile is the only one with keys past the query (and the
+      // only one that can hold rows past the sequence, repeated rows that
+      // the same mask removes)
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -482,13 +562,13 @@ attn_fwd_kernel(KParams P) {
         const bf16x8 pa = as_bf16x8(pk);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(pa, read_tr(sm.t.b, ST, 32 * wj + 16 * ks + 4 * g, 32 * db, lane),
+          oacc[db] = mfma32(pa, sread_tr<D>(vt_lds, 32 * wj + 16 * ks + 4 * g, 32 * db, lane),
                             oacc[db]);
       }
     }
 
     // sum the two key halves, store O (bf16)
-    sum_store_tile<D>(&sm.red[0][0], oacc, wj == 0, wi, g, l32, tid,
+    sum_store_tile<D>(sm.red, oacc, wj == 0, wi, g, l32, tid,
                       P.out0 + ((si.start + (int64_t)qt * TILE) * P.H + h) * D,
                       row_stride, q_valid);
   }
@@ -988,7 +1068,8 @@ int persistent_grid(K kernel, size_t dyn, int64_t items, int dev) {
 // this budget (staged once per work-group), else a single per-item slot.
 constexpr size_t ALL_HEADS_BUDGET = 32 * 1024;
 bool all_heads(const Problem &p) {
-  return p.has_time && sizeof(float) * (size_t)p.H * (KTAB + p.nb) <= ALL_HEADS_BUDGET;
+  const size_t budget = p.d == 64 ? ALL_HEADS_BUDGET : ALL_HEADS_BUDGET / 4;
+  return p.has_time && sizeof(float) * (size_t)p.H * (KTAB + p.nb) <= budget;
 }
 size_t slots_bytes(const Problem &p) {
   if (!p.has_time) return 0;
