@@ -237,13 +237,16 @@ int hstu_jagged_schedule(const int64_t *seq_offsets, int32_t B,
   hipError_t e = launch_schedule(seq_offsets, p, workspace, L, s);
   if (e != hipSuccess) return hip_fail(e, "schedule launch");
   const char *ws = (const char *)workspace;
-  const size_t list_bytes = sizeof(WorkEntry) * (size_t)p.max_entries;
+  // the exported lists are the (sequence, tile) pairs of the entries
+  const size_t rows = (size_t)p.max_entries;
   e = hipMemcpyAsync(n_entries, ws + L.ctrl + sizeof(int32_t) * CTRL_N_ENTRIES,
                      sizeof(int32_t), hipMemcpyDeviceToDevice, s);
-  if (e == hipSuccess && list_bytes)
-    e = hipMemcpyAsync(list_q, ws + L.list_q, list_bytes, hipMemcpyDeviceToDevice, s);
-  if (e == hipSuccess && list_bytes)
-    e = hipMemcpyAsync(list_k, ws + L.list_k, list_bytes, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && rows)
+    e = hipMemcpy2DAsync(list_q, 2 * sizeof(int32_t), ws + L.list_q, sizeof(WorkEntry),
+                         2 * sizeof(int32_t), rows, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && rows)
+    e = hipMemcpy2DAsync(list_k, 2 * sizeof(int32_t), ws + L.list_k, sizeof(WorkEntry),
+                         2 * sizeof(int32_t), rows, hipMemcpyDeviceToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "work-list copy");
   return HSTU_OK;
 }

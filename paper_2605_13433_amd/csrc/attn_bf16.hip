@@ -50,6 +50,8 @@ constexpr int RM_PAD = 8;        // row-major LDS stride D+8 bf16
 constexpr int POS_COPY = 2 * TILE + 4;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
+constexpr float L2E = 1.44269504088896341f;      // log2(e)
+constexpr float LN2 = 0.693147180559945309f;     // 1 / log2(e)
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -153,7 +155,8 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
 __device__ __forceinline__ float pos_fetch(const KParams &P, int h, int qt, int kt, int tid) {
   const int span = 2 * P.N - 1;
   const int idx = (kt - qt) * TILE + P.N - TILE + tid;
-  return (tid < 2 * TILE - 1 && idx >= 0 && idx < span) ? P.pos_w[(int64_t)h * span + idx] : 0.0f;
+  return (tid < 2 * TILE - 1 && idx >= 0 && idx < span)
+             ? L2E * P.pos_w[(int64_t)h * span + idx] : 0.0f;
 }
 
 template <bool REVERSED>
@@ -173,9 +176,10 @@ __device__ __forceinline__ const float *pos_lane(const float *pos, int x0) {
   return pos + s * POS_COPY + (x0 - s);
 }
 
-// Float-exponent index of an exact |delta| < 2^24 (see file comment).
-__device__ __forceinline__ int time_index(int32_t delta) {
-  return (int)__builtin_amdgcn_ubfe(__float_as_uint((float)delta), 21u, 10u);
+// Float-exponent index of a time difference held exactly in a float
+// (|delta| < 2^24; see file comment).  The sign bit is not in the field.
+__device__ __forceinline__ int time_index(float delta) {
+  return (int)__builtin_amdgcn_ubfe(__float_as_uint(delta), 21u, 10u);
 }
 
 // Bucket of float-exponent index k (k = 0 <-> 0; 508, 512, 514 <-> 1, 2, 3;
@@ -186,16 +190,17 @@ __device__ __forceinline__ int bucket_of_index(int k, int nb) {
   return b < nb - 1 ? b : nb - 1;
 }
 
-// silu(x) / N = x / (N (1 + e^-x)); hardware exp2 and reciprocal.
-__device__ __forceinline__ float silu_over_n(float x, float n) {
-  const float t = __builtin_amdgcn_exp2f(x * -1.44269504088896341f);
-  return x * __builtin_amdgcn_rcpf(__builtin_fmaf(n, t, n));
+// Scores are handled in the base-2 domain x' = x log2(e): the MFMA result is
+// scaled once and the bias tables are staged pre-scaled, so that e^-x is a
+// single exp2 of -x'.
+//   silu(x) / N = x' / (N log2e (1 + 2^-x'));  nl = N log2e
+__device__ __forceinline__ float silu2_over_n(float xs, float nl) {
+  const float t = __builtin_amdgcn_exp2f(-xs);
+  return xs * __builtin_amdgcn_rcpf(__builtin_fmaf(nl, t, nl));
 }
 
-// silu'(x) / N = sigma(x) (1 + x (1 - sigma(x))) / N
-__device__ __forceinline__ float dsilu_over_n(float x, float inv_n) {
-  const float sg = sigmoid_f(x);
-  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * inv_n;
+__device__ __forceinline__ float sigmoid2(float xs) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-xs));
 }
 
 template <int D>
@@ -208,7 +213,7 @@ struct StreamSmem {
     float red[2][32 * D];                // cross-wave sums at the end of an item
   };
   alignas(16) float pos[4 * POS_COPY];
-  alignas(16) int32_t ts32[TILE];        // streamed-tile timestamps - ts_start
+  alignas(16) float ts32[TILE];          // streamed-tile timestamps - ts_start
   int64_t ts64[TILE];                    // raw streamed-tile timestamps
   int flag[2];                           // "some timestamp is far" (parity-buffered)
   int item;
@@ -261,8 +266,8 @@ __device__ __forceinline__ int time_slot_floats(const KParams &P) { return KTAB 
 
 __device__ __forceinline__ void stage_time_head(const KParams &P, float *slot, int h, int tid) {
   const float *tab = P.time_w + (int64_t)h * P.nb;
-  for (int x = tid; x < KTAB; x += THREADS) slot[x] = tab[bucket_of_index(x, P.nb)];
-  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = tab[x];
+  for (int x = tid; x < KTAB; x += THREADS) slot[x] = L2E * tab[bucket_of_index(x, P.nb)];
+  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = L2E * tab[x];
 }
 
 // Kernel start: every head's tables when they fit (then no per-item staging).
@@ -284,14 +289,14 @@ __device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, i
 // c_row(r, g), columns 32*db + l32).  The writer wave stores its blocks to
 // LDS, its partner adds its own in place, then every thread converts 8
 // consecutive floats of one
-// row and writes them as a single 16-byte chunk; rows at or beyond `valid`
-// are not written.  (The partner reads, adds and writes back its own
+// row, scales them by `scale` and writes them as a single 16-byte chunk;
+// rows at or beyond `valid` are not written.  (The partner reads, adds and writes back its own
 // addresses: LDS float atomics are far slower here even without conflicts.)
 template <int D>
 __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D / 32],
                                                bool writer, int half, int g, int l32,
                                                int tid, u16 *__restrict__ out,
-                                               int row_stride, int valid) {
+                                               int row_stride, int valid, float scale) {
   lds_barrier();
   if (writer) {
 #pragma unroll
@@ -318,10 +323,10 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
       const float4 a = *(const float4 *)(red + row * D + 8 * c8);
       const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
       uint4 pk;
-      pk.x = pack2(a.x, a.y);
-      pk.y = pack2(a.z, a.w);
-      pk.z = pack2(b.x, b.y);
-      pk.w = pack2(b.z, b.w);
+      pk.x = pack2(scale * a.x, scale * a.y);
+      pk.y = pack2(scale * a.z, scale * a.w);
+      pk.z = pack2(scale * b.x, scale * b.y);
+      pk.w = pack2(scale * b.z, scale * b.w);
       *(uint4 *)(out + row * row_stride + 8 * c8) = pk;
     }
   }
@@ -386,40 +391,95 @@ __device__ __forceinline__ bf16x8 sread_tr(const u16 *lds, int krow, int ncol, i
 
 // Forward shared memory: two K/V buffers (tile kt computes from one while
 // tile kt+1 streams into the other), per-parity bias slices, a three-slot
-// "far timestamp" flag.  The cross-wave output sum reuses the tile buffers.
+// "far timestamp" flag.  An item's output is summed across waves in the
+// buffer of its last tile.
 template <int D>
 struct FwdSmem {
-  union {
-    u16 tile[2][2][TILE * D];            // [buffer][K, V]
-    float red[TILE * D];
-  };
+  u16 tile[2][2][TILE * D];              // [buffer][K, V]
   alignas(16) float pos[2][4 * POS_COPY];
-  alignas(16) int32_t ts32[2][TILE];
+  alignas(16) float ts32[2][TILE];
   int64_t ts64[2][TILE];
   int flag[3];
-  int item;
+  int next[2];                           // item index published by thread 0,
+                                         // by parity of the publishing item
 };
+
+// A work-list item decoded: sequence start and length, tile, head and (in
+// the backward list) the dQ flag.
+struct Item {
+  int64_t start;
+  int32_t len, tile, h, dq;
+};
+
+__device__ __forceinline__ Item load_item(const KParams &P, int idx) {
+  const WorkEntry e = P.list[idx / P.H];
+  Item it;
+  it.start = e.start;
+  it.len = e.len;
+  it.tile = e.tile & ~BWD_DQ_FLAG;
+  it.dq = e.tile & BWD_DQ_FLAG;
+  it.h = idx % P.H;
+  return it;
+}
+
+// Streams an item's first key tile into (kbuf, vbuf) and fetches its bias
+// slice and timestamps into registers.  Timestamps of rows past the
+// sequence repeat its last row (those rows are always masked).
+template <int D, bool POS, bool TIME>
+__device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it, u16 *kbuf,
+                                               u16 *vbuf, int w, int lane, int tid, int i_loc,
+                                               int row_stride, int64_t &ts_start,
+                                               int64_t &ts_i, int64_t &ts_k, float &pos_v) {
+  const int64_t hb = (it.start * P.H + it.h) * D;
+  dma_tile<D>(P.k + hb, it.len, row_stride, kbuf, w, lane);
+  dma_tile<D>(P.v + hb, it.len, row_stride, vbuf, w, lane);
+  if (TIME) {
+    const int q_valid = it.len - it.tile * TILE;
+    ts_start = P.ts[it.start];
+    ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
+    if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
+  }
+  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid);
+}
 
 // ---------------------------------------------------------------- forward
 // One work-group barrier per key tile: the barrier of tile kt publishes its
 // DMA-filled buffers and bias slices, and proves every wave is done with
-// tile kt-1, whose buffer then takes tile kt+1.
+// tile kt-1, whose buffer then takes tile kt+1.  Items are pipelined: each
+// work-group's first two items are static (the list's head, longest first),
+// the pop for the item after next is issued when an item starts, and an
+// item's last tile streams the next item's first key tile, query rows, bias
+// slice and timestamps, so no item starts with an exposed memory latency.
 template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, 2)
 attn_fwd_kernel(KParams P) {
   __shared__ FwdSmem<D> sm;
   extern __shared__ float dyn[];              // time tables (see item_time_slot)
-  const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
+  int cur = blockIdx.x;
+  int nxt = gridDim.x + blockIdx.x;
+  if (cur >= n_items) return;
+  const int tid0 = threadIdx.x;
   if (tid0 < 3) sm.flag[tid0] = 0;
   if (TIME) stage_all_heads(P, dyn, tid0);
   int phase = 0;
 
+  Item it = load_item(P, cur);
+  int item_no = 0;                            // items done by this work-group
+  int64_t ts_start = 0, ts_i = 0, ts_k = 0;
+  float pos_v = 0.0f;
+  bf16x8 qreg[D / 16];
+  {
+    const int lane = tid0 & 63, g = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid0 >> 6);
+    const int i_loc = 32 * (w & 1) + l32;
+    fwd_item_start<D, POS, TIME>(P, it, sm.tile[0][0], sm.tile[0][1], w, lane, tid0, i_loc,
+                                 P.H * D, ts_start, ts_i, ts_k, pos_v);
+    load_stationary<D>(P.q + ((it.start + (int64_t)it.tile * TILE) * P.H + it.h) * D, i_loc,
+                       it.len - it.tile * TILE, P.H * D, g, qreg);
+  }
+
   for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
     // Lane-derived values are rebuilt per item from an opaque copy of the
     // thread index: otherwise the compiler hoists dozens of per-lane
     // addresses out of the persistent loop and pins their registers.
@@ -430,36 +490,26 @@ attn_fwd_kernel(KParams P) {
     const int lane = tid & 63, g = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wi = w & 1, wj = w >> 1;        // query half, key half
-
-    const WorkEntry e = P.list[item / P.H];
-    const int h = item % P.H;
-    const SeqInfo si = P.info[e.seq];
-    const int qt = e.tile;
-    const int q_valid = si.len - qt * TILE;
+    const int qt = it.tile, h = it.h;
+    const int q_valid = it.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
-    const u16 *qbase = P.q + ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
-    const u16 *kbase = P.k + (si.start * P.H + h) * D;
-    const u16 *vbase = P.v + (si.start * P.H + h) * D;
 
-    // key tile 0 starts streaming before anything else
-    dma_tile<D>(kbase, si.len, row_stride, sm.tile[phase & 1][0], w, lane);
-    dma_tile<D>(vbase, si.len, row_stride, sm.tile[phase & 1][1], w, lane);
-
-    bf16x8 qreg[D / 16];
-    load_stationary<D>(qbase, i_loc, q_valid, row_stride, g, qreg);
-
-    int64_t ts_start = 0, ts_i = 0;
-    int32_t ts_i32 = 0;
+    float ts_i32 = 0.0f;
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
-      ts_start = P.ts[si.start];
-      ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
-      ts_i32 = (int32_t)rel;
+      ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
       ktab = item_time_slot(P, dyn, h, tid);
     }
+    const int64_t ts_i_item = ts_i, ts_start_item = ts_start;
+
+    int nxt2 = 0;
+    if (tid == 0) nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
+    const bool has_next = nxt < n_items;
+    Item nit = it;
+    if (has_next) nit = load_item(P, nxt);
 
     f32x16 oacc[D / 32];
 #pragma unroll
@@ -467,35 +517,36 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
 
-    int64_t ts_k = 0;
-    float pos_v = 0.0f;
-    if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
-    if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
-
     for (int kt = 0; kt <= qt; ++kt, ++phase) {
       const int pb = phase & 1, fs = phase % 3;
+      const bool last = kt == qt;
       if (POS) pos_store<false>(pos_v, sm.pos[pb], tid);
       if (TIME) {
         bool far = q_far;
         if (tid < TILE) {
-          const int64_t rel = ts_k - ts_start;
-          sm.ts32[pb][tid] = (int32_t)rel;
+          const int64_t rel = ts_k - ts_start_item;
+          sm.ts32[pb][tid] = (float)(int32_t)rel;
           sm.ts64[pb][tid] = ts_k;
           far |= rel >= NEAR || rel <= -NEAR;
         }
         if (far) sm.flag[fs] = 1;
       }
+      if (last && tid == 0) sm.next[item_no & 1] = nxt2;
       wait_vm();
       lds_barrier();
       const bool slow = TIME && sm.flag[fs] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 2) % 3] = 0;
-      if (kt < qt) {       // stream the next key tile into the other buffer
-        const int k_valid = si.len - (kt + 1) * TILE;
-        const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
+      if (!last) {         // stream the next key tile into the other buffer
+        const int k_valid = it.len - (kt + 1) * TILE;
+        const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
         dma_tile<D>(P.k + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][0], w, lane);
         dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
-        if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
+        if (TIME && tid < TILE)
+          ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
+      } else if (has_next) {   // ... or the next item's first one
+        fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
+                                     tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
       }
       const u16 *kt_lds = sm.tile[pb][0];
       const u16 *vt_lds = sm.tile[pb][1];
@@ -507,26 +558,32 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks)
         s = mfma32(sread_rm<D>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
+      if (last && has_next)    // the query rows are free: fetch the next item's
+        load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
+                           i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
 
-      // bias: this lane's keys sit at 32 wj + 4 g + 8 q4 + c
+      // x' = s log2e + bias'; this lane's keys sit at 32 wj + 4 g + 8 q4 + c
       float x[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = s[r];
       const int kb = 32 * wj + 4 * g;
       if (POS) {
         const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const float4 pbv = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pbv.x; x[4 * q4 + 1] += pbv.y;
-          x[4 * q4 + 2] += pbv.z; x[4 * q4 + 3] += pbv.w;
+          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pbv.x);
+          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pbv.y);
+          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pbv.z);
+          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pbv.w);
         }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
       }
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32[pb] + kb + 8 * q4);
+            const float4 t4 = *(const float4 *)(sm.ts32[pb] + kb + 8 * q4);
             x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
             x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
             x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
@@ -535,17 +592,17 @@ attn_fwd_kernel(KParams P) {
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[pb][kb + c_row(r, 0)], P.nb)];
+            x[r] += ktab[KTAB + time_bucket(ts_i_item - sm.ts64[pb][kb + c_row(r, 0)], P.nb)];
         }
       }
-      const float fN = (float)P.N;
+      const float nl = (float)P.N * L2E;
       float av[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) av[r] = silu_over_n(x[r], fN);
+      for (int r = 0; r < 16; ++r) av[r] = silu2_over_n(x[r], nl);
       // the diagonal tile is the only one with keys past the query (and the
       // only one that can hold rows past the sequence, repeated rows that
       // the same mask removes)
-      if (kt == qt) {
+      if (last) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (kb + c_row(r, 0) > i_loc) av[r] = 0.0f;
@@ -567,10 +624,15 @@ attn_fwd_kernel(KParams P) {
       }
     }
 
-    // sum the two key halves, store O (bf16)
-    sum_store_tile<D>(sm.red, oacc, wj == 0, wi, g, l32, tid,
-                      P.out0 + ((si.start + (int64_t)qt * TILE) * P.H + h) * D,
-                      row_stride, q_valid);
+    // sum the two key halves in the last tile's buffer, store O (bf16)
+    sum_store_tile<D>((float *)sm.tile[(phase - 1) & 1], oacc, wj == 0, wi, g, l32, tid,
+                      P.out0 + ((it.start + (int64_t)qt * TILE) * P.H + h) * D,
+                      row_stride, q_valid, 1.0f);
+    if (!has_next) break;
+    cur = nxt;
+    it = nit;
+    nxt = sm.next[item_no & 1];
+    ++item_no;
   }
 }
 
@@ -601,14 +663,14 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     load_stationary<D>(P.dO + qoff, i_loc, q_valid, row_stride, g, doreg);
 
     int64_t ts_start = 0, ts_i = 0;
-    int32_t ts_i32 = 0;
+    float ts_i32 = 0.0f;
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
-      ts_i32 = (int32_t)rel;
+      ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
       ktab = item_time_slot(P, dyn, h, tid);
     }
@@ -638,7 +700,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
-          sm.ts32[tid] = (int32_t)rel;
+          sm.ts32[tid] = (float)(int32_t)rel;
           sm.ts64[tid] = ts_k;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -666,23 +728,26 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       }
 
       float x[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = s[r];
       const int kb = 32 * wj + 4 * g;
       if (POS) {
         const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
-          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pb.x);
+          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pb.y);
+          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pb.z);
+          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pb.w);
         }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
       }
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
+            const float4 t4 = *(const float4 *)(sm.ts32 + kb + 8 * q4);
             x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
             x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
             x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
@@ -694,9 +759,14 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
             x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
       }
+      // dS N = dA silu'(x) = dA (sg + x sg (1 - sg)); the 1/N goes on dQ
       float dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu_over_n(x[r], P.inv_n);
+      for (int r = 0; r < 16; ++r) {
+        const float sg = sigmoid2(x[r]);
+        const float u = (x[r] * LN2) * sg;
+        dsv[r] = da[r] * __builtin_fmaf(u, 1.0f - sg, sg);
+      }
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -719,7 +789,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     }
 
     sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
-                      row_stride, q_valid);
+                      row_stride, q_valid, P.inv_n);
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -772,14 +842,14 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
 
     int64_t ts_start = 0, ts_j = 0;
-    int32_t ts_j32 = 0;
+    float ts_j32 = 0.0f;
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_j = j_loc < k_valid ? P.ts[si.start + (int64_t)kt * TILE + j_loc] : ts_start;
       const int64_t rel = ts_j - ts_start;
-      ts_j32 = (int32_t)rel;
+      ts_j32 = (float)(int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
       ktab = item_time_slot(P, dyn, h, tid);
     }
@@ -816,7 +886,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         bool far = k_far;
         if (tid < TILE) {
           const int64_t rel = ts_q - ts_start;
-          sm.ts32[tid] = (int32_t)rel;
+          sm.ts32[tid] = (float)(int32_t)rel;
           sm.ts64[tid] = ts_q;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -850,23 +920,26 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       const int ib = 32 * wi + 4 * g;
       const int x0 = j_loc - ib + (TILE - 1);
       float x[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = s[r];
       if (POS) {
         const float *pl = pos_lane(sm.pos, 2 * TILE - 2 - x0);
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
-          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
+          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pb.x);
+          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pb.y);
+          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pb.z);
+          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pb.w);
         }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
       }
       int tk[16];
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * q4);
+            const float4 t4 = *(const float4 *)(sm.ts32 + ib + 8 * q4);
             tk[4 * q4 + 0] = time_index(t4.x - ts_j32);
             tk[4 * q4 + 1] = time_index(t4.y - ts_j32);
             tk[4 * q4 + 2] = time_index(t4.z - ts_j32);
@@ -882,17 +955,18 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
           }
         }
       }
-      // a = silu(x)/N, dS = dA silu'(x)/N = dA (sg + a' (1 - sg))/N with
-      // a' = x sg.  Query rows past the sequence have dO = 0, hence dA = 0
-      // and dS = 0, and contribute a * 0 to dV: only the diagonal tile
-      // needs a mask (the causal one).
+      // N a = silu(x) = x sg, N dS = dA silu'(x) = dA (sg + a1 (1 - sg))
+      // with a1 = x sg; the 1/N goes on dK, dV and the tables at the end.
+      // Query rows past the sequence have dO = 0, hence dA = 0 and dS = 0,
+      // and contribute a * 0 to dV: only the diagonal tile needs a mask
+      // (the causal one).
       float av[16], dsv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float sg = sigmoid_f(x[r]);
-        const float a1 = x[r] * sg;
-        av[r] = a1 * P.inv_n;
-        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1) * P.inv_n;
+        const float sg = sigmoid2(x[r]);
+        const float a1 = (x[r] * LN2) * sg;
+        av[r] = a1;
+        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1);
       }
       if (qt == kt) {
 #pragma unroll
@@ -988,9 +1062,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
-                      row_stride, k_valid);
+                      row_stride, k_valid, P.inv_n);
     sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
-                      row_stride, k_valid);
+                      row_stride, k_valid, P.inv_n);
 }
 
 // Backward: one persistent launch over the combined list, whose entries are

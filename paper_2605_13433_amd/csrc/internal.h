@@ -36,11 +36,16 @@ struct SeqInfo {
   int32_t ntiles;
 };
 
-// One work-list entry: a sequence and a 64-row tile index inside it.  The
-// heads of an entry are expanded by the consumer (item = entry * H + h).
+// One work-list entry: a sequence and a 64-row tile index inside it, with
+// the sequence's clamped start row and length copied in, so that a consumer
+// needs one load per entry.  The heads of an entry are expanded by the
+// consumer (item = entry * H + h).
 struct WorkEntry {
   int32_t seq;
   int32_t tile;
+  int32_t len;
+  int32_t reserved;
+  int64_t start;
 };
 
 // In the combined backward list, dQ entries carry this bit in `tile`

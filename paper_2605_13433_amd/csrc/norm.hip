@@ -167,7 +167,8 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 //     work-groups folded theirs into.  Block = 64 consecutive (h, k)
 //     columns; waves stride over the bins.
 // Summation order is fixed, so the result is deterministic given the
-// partials.
+// partials.  The attention backward accumulates N dS (the 1/N is applied
+// here, once per table entry).
 constexpr int FIN_THREADS = 1024;
 constexpr int FIN_WAVES = FIN_THREADS / 64;
 
@@ -176,7 +177,7 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
                        const float *__restrict__ pos_part, int H, int N,
                        float *__restrict__ d_pos, int pos_blocks,
                        const float *__restrict__ time_part, int n_parts,
-                       int width, float *__restrict__ d_time) {
+                       int width, float *__restrict__ d_time, float scale) {
   __shared__ float red[FIN_WAVES][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   float acc = 0.0f;
@@ -209,7 +210,7 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
       float s = 0.0f;
       for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
       const int64_t span = 2 * (int64_t)N - 1;
-      d_pos[h * span + (N - 1 - m)] = s;
+      d_pos[h * span + (N - 1 - m)] = scale * s;
       if (N + m < span) d_pos[h * span + N + m] = 0.0f;
     }
   } else {
@@ -221,7 +222,7 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
     if (wv == 0 && c < width) {
       float s = 0.0f;
       for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
-      d_time[c] = s;
+      d_time[c] = scale * s;
     }
   }
 }
@@ -273,7 +274,7 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                      d_pos ? (const float *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
                      d_pos, pos_blocks,
                      d_time ? (const float *)(ws + a.L.dtime_part) : nullptr,
-                     DTIME_BINS, width, d_time);
+                     DTIME_BINS, width, d_time, 1.0f / (float)p.N);
   return hipGetLastError();
 }
 

@@ -104,21 +104,25 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
   __syncthreads();
 
   for (int b = tid; b < a.B; b += NT) {
-    const int nt = a.info[b].ntiles;
+    const SeqInfo si = a.info[b];
+    const int nt = si.ntiles;
     for (int t = 0; t < nt; ++t) {
+      const WorkEntry we{b, t, si.len, 0, si.start};
+      WorkEntry wq = we;
+      wq.tile |= BWD_DQ_FLAG;
       const int cq = t + 1;          // q-tile t visits k-tiles 0..t
       const int ck = nt - t;         // k-tile t is visited by q-tiles t..nt-1
       const int sq = sm.start[cq] + atomicAdd(&sm.fill_q[cq], 1);
       const int sk = sm.start[ck] + atomicAdd(&sm.fill_k[ck], 1);
-      if (sq < a.cap) a.list_q[sq] = WorkEntry{b, t};
-      if (a.list_k && sk < a.cap) a.list_k[sk] = WorkEntry{b, t};
+      if (sq < a.cap) a.list_q[sq] = we;
+      if (a.list_k && sk < a.cap) a.list_k[sk] = we;
       if (a.list_b) {
         // combined backward list: bin c spans 2 ge[c] slots from 2 start[c],
         // dK/dV entries first (the heavier item of equal cost), then dQ ones
         const int bk = sk + sm.start[ck];
         const int bq = sq + sm.start[cq] + sm.ge[cq];
-        if (bk < 2 * a.cap) a.list_b[bk] = WorkEntry{b, t};
-        if (bq < 2 * a.cap) a.list_b[bq] = WorkEntry{b, t | BWD_DQ_FLAG};
+        if (bk < 2 * a.cap) a.list_b[bk] = we;
+        if (bq < 2 * a.cap) a.list_b[bq] = wq;
       }
     }
   }
