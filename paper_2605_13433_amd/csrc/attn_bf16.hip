@@ -46,12 +46,11 @@ namespace hstu {
 namespace {
 
 constexpr int THREADS = 256;     // 4 waves
-constexpr int RM_PAD = 8;        // row-major LDS stride D+8 bf16
+constexpr int RM_PAD = 8;        // backward: row-major LDS stride D+8 bf16
 constexpr int POS_COPY = 2 * TILE + 4;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
 constexpr float L2E = 1.44269504088896341f;      // log2(e)
-constexpr float LN2 = 0.693147180559945309f;     // 1 / log2(e)
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -72,63 +71,6 @@ struct KParams {
   float inv_n;
   int32_t all_heads;      // time tables of every head staged once per work-group
 };
-
-// ------------------------------------------------------------ tile staging
-// A 64-row tile of one head, D bf16 per row, moved global -> registers ->
-// LDS in 16-byte chunks; rows at or beyond `valid` are zeros, so padded
-// keys/queries contribute exact zeros to every product.
-template <int D>
-struct TileRegs {
-  static constexpr int CPT = TILE * D / 8 / THREADS;   // chunks per thread
-  uint4 c[CPT];
-
-  __device__ __forceinline__ void load(const u16 *__restrict__ tile_base,
-                                       int valid, int row_stride, int tid) {
-    if (valid >= TILE) {
-#pragma unroll
-      for (int x = 0; x < CPT; ++x) {
-        const int ch = tid + THREADS * x;
-        c[x] = *(const uint4 *)(tile_base + (ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8);
-      }
-    } else {
-#pragma unroll
-      for (int x = 0; x < CPT; ++x) {
-        const int ch = tid + THREADS * x;
-        const int r = ch / (D / 8);
-        c[x] = r < valid ? *(const uint4 *)(tile_base + r * row_stride + (ch % (D / 8)) * 8)
-                         : make_uint4(0, 0, 0, 0);
-      }
-    }
-  }
-  __device__ __forceinline__ void store(u16 *lds, int tid) const {
-#pragma unroll
-    for (int x = 0; x < CPT; ++x) {
-      const int ch = tid + THREADS * x;
-      *(uint4 *)(lds + (ch / (D / 8)) * (D + RM_PAD) + (ch % (D / 8)) * 8) = c[x];
-    }
-  }
-};
-
-// 8 consecutive bf16 of row `row` of a row-major LDS tile, from column col.
-__device__ __forceinline__ bf16x8 read_rm(const u16 *lds, int stride, int row, int col) {
-  return *(const bf16x8 *)(lds + row * stride + col);
-}
-
-// Operand holding, for lane l, column ncol + (l & 31) of rows krow .. krow+3
-// and krow+8 .. krow+11 of a row-major LDS tile (krow already includes this
-// lane's 4*(l/32)), via two LDS transpose loads.  Within a 16-lane group,
-// lane c addresses row (c>>2), columns 4*(c&3)..+3 of its group's 16-column
-// slab; the transpose hands lane i the column slab+i of the four rows.
-__device__ __forceinline__ bf16x8 read_tr(const u16 *lds, int stride, int krow,
-                                          int ncol, int lane) {
-  const int c = lane & 15;
-  const u16 *p = lds + (krow + (c >> 2)) * stride + ncol + ((lane >> 4) & 1) * 16 + 4 * (c & 3);
-  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
-  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 8 * stride));
-  typedef short v8i16 __attribute__((ext_vector_type(8)));
-  const v8i16 x = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return __builtin_bit_cast(bf16x8, x);
-}
 
 // Stationary 32-row operand: lane holds row `row` of the tile (zero when
 // row >= valid), dims 16*ks + 8*g .. +7, ks = 0 .. D/16-1.
@@ -152,11 +94,13 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
 // entry x - s) for the q-stationary kernels, reversed order (copy s, entry
 // 126 - x - s) for the k-stationary one, whose lanes walk the offsets
 // downwards.  Threads with nothing to store write a never-read pad slot.
-__device__ __forceinline__ float pos_fetch(const KParams &P, int h, int qt, int kt, int tid) {
+// The entry is multiplied by `scale` (log2 e in the forward's base-2 domain).
+__device__ __forceinline__ float pos_fetch(const KParams &P, int h, int qt, int kt, int tid,
+                                           float scale) {
   const int span = 2 * P.N - 1;
   const int idx = (kt - qt) * TILE + P.N - TILE + tid;
   return (tid < 2 * TILE - 1 && idx >= 0 && idx < span)
-             ? L2E * P.pos_w[(int64_t)h * span + idx] : 0.0f;
+             ? scale * P.pos_w[(int64_t)h * span + idx] : 0.0f;
 }
 
 template <bool REVERSED>
@@ -199,26 +143,6 @@ __device__ __forceinline__ float silu2_over_n(float xs, float nl) {
   return xs * __builtin_amdgcn_rcpf(__builtin_fmaf(nl, t, nl));
 }
 
-__device__ __forceinline__ float sigmoid2(float xs) {
-  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-xs));
-}
-
-template <int D>
-struct StreamSmem {
-  union {
-    struct {
-      u16 a[TILE * (D + RM_PAD)];
-      u16 b[TILE * (D + RM_PAD)];
-    } t;
-    float red[2][32 * D];                // cross-wave sums at the end of an item
-  };
-  alignas(16) float pos[4 * POS_COPY];
-  alignas(16) float ts32[TILE];          // streamed-tile timestamps - ts_start
-  int64_t ts64[TILE];                    // raw streamed-tile timestamps
-  int flag[2];                           // "some timestamp is far" (parity-buffered)
-  int item;
-};
-
 // d_time is accumulated in LDS as 64-bit fixed point (value * 2^24) with
 // integer atomics: LDS float atomics cost hundreds of cycles per wave
 // instruction here, integer ones do not.  Range: each added run sum below
@@ -237,26 +161,6 @@ __device__ __forceinline__ float from_fixed(fix64 v) {
   return (float)((double)(long long)v * (1.0 / 16777216.0));
 }
 
-// Per-lane running sum of d_time contributions over one time index (the
-// lane's pairs visit non-decreasing indices when timestamps are ordered, so
-// a run is flushed only when its index changes).
-struct TimeRun {
-  float sum = 0.0f;
-  int cur = -1;
-  __device__ __forceinline__ void add(fix64 *acc, int k, float v) {
-    if (k != cur) {
-      if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
-      cur = k;
-      sum = 0.0f;
-    }
-    sum += v;
-  }
-  __device__ __forceinline__ void flush(fix64 *acc) {
-    if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
-    cur = -1;
-    sum = 0.0f;
-  }
-};
 
 
 // Time tables in dynamic LDS, one slot per head (or a single slot restaged
@@ -264,22 +168,25 @@ struct TimeRun {
 // then the nb raw buckets for the exact path.
 __device__ __forceinline__ int time_slot_floats(const KParams &P) { return KTAB + P.nb; }
 
-__device__ __forceinline__ void stage_time_head(const KParams &P, float *slot, int h, int tid) {
+__device__ __forceinline__ void stage_time_head(const KParams &P, float *slot, int h, int tid,
+                                                float scale) {
   const float *tab = P.time_w + (int64_t)h * P.nb;
-  for (int x = tid; x < KTAB; x += THREADS) slot[x] = L2E * tab[bucket_of_index(x, P.nb)];
-  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = L2E * tab[x];
+  for (int x = tid; x < KTAB; x += THREADS) slot[x] = scale * tab[bucket_of_index(x, P.nb)];
+  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = scale * tab[x];
 }
 
 // Kernel start: every head's tables when they fit (then no per-item staging).
-__device__ __forceinline__ void stage_all_heads(const KParams &P, float *dyn, int tid) {
+__device__ __forceinline__ void stage_all_heads(const KParams &P, float *dyn, int tid,
+                                                float scale) {
   if (!P.all_heads) return;
-  for (int h = 0; h < P.H; ++h) stage_time_head(P, dyn + h * time_slot_floats(P), h, tid);
+  for (int h = 0; h < P.H; ++h) stage_time_head(P, dyn + h * time_slot_floats(P), h, tid, scale);
 }
 
 // Item start: the slot of head h (staged now if tables are per item).
-__device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, int h, int tid) {
+__device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, int h, int tid,
+                                                 float scale) {
   if (P.all_heads) return dyn + h * time_slot_floats(P);
-  stage_time_head(P, dyn, h, tid);
+  stage_time_head(P, dyn, h, tid, scale);
   return dyn;
 }
 
@@ -439,7 +346,7 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
     ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid);
+  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, L2E);
 }
 
 // ---------------------------------------------------------------- forward
@@ -461,7 +368,7 @@ attn_fwd_kernel(KParams P) {
   if (cur >= n_items) return;
   const int tid0 = threadIdx.x;
   if (tid0 < 3) sm.flag[tid0] = 0;
-  if (TIME) stage_all_heads(P, dyn, tid0);
+  if (TIME) stage_all_heads(P, dyn, tid0, L2E);
   int phase = 0;
 
   Item it = load_item(P, cur);
@@ -501,7 +408,7 @@ attn_fwd_kernel(KParams P) {
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid, L2E);
     }
     const int64_t ts_i_item = ts_i, ts_start_item = ts_start;
 
@@ -543,7 +450,7 @@ attn_fwd_kernel(KParams P) {
         dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, L2E);
       } else if (has_next) {   // ... or the next item's first one
         fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
                                      tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
@@ -636,6 +543,118 @@ attn_fwd_kernel(KParams P) {
   }
 }
 
+// ------------------------------------------------------------ backward
+// The backward kernel stages its streamed tiles through registers into a
+// padded row-major LDS tile (measured faster here than the forward's
+// DMA-filled buffers: the backward is register-bound and the staging
+// overlaps with its longer tile step) and works in natural units with
+// 1/N applied per element.
+
+// A 64-row tile of one head, D bf16 per row, moved global -> registers ->
+// LDS in 16-byte chunks; rows at or beyond `valid` are zeros, so padded
+// keys/queries contribute exact zeros to every product.
+template <int D>
+struct TileRegs {
+  static constexpr int CPT = TILE * D / 8 / THREADS;   // chunks per thread
+  uint4 c[CPT];
+
+  __device__ __forceinline__ void load(const u16 *__restrict__ tile_base,
+                                       int valid, int row_stride, int tid) {
+    if (valid >= TILE) {
+#pragma unroll
+      for (int x = 0; x < CPT; ++x) {
+        const int ch = tid + THREADS * x;
+        c[x] = *(const uint4 *)(tile_base + (ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8);
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < CPT; ++x) {
+        const int ch = tid + THREADS * x;
+        const int r = ch / (D / 8);
+        c[x] = r < valid ? *(const uint4 *)(tile_base + r * row_stride + (ch % (D / 8)) * 8)
+                         : make_uint4(0, 0, 0, 0);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(u16 *lds, int tid) const {
+#pragma unroll
+    for (int x = 0; x < CPT; ++x) {
+      const int ch = tid + THREADS * x;
+      *(uint4 *)(lds + (ch / (D / 8)) * (D + RM_PAD) + (ch % (D / 8)) * 8) = c[x];
+    }
+  }
+};
+
+// 8 consecutive bf16 of row `row` of a row-major LDS tile, from column col.
+__device__ __forceinline__ bf16x8 read_rm(const u16 *lds, int stride, int row, int col) {
+  return *(const bf16x8 *)(lds + row * stride + col);
+}
+
+// Operand holding, for lane l, column ncol + (l & 31) of rows krow .. krow+3
+// and krow+8 .. krow+11 of a row-major LDS tile (krow already includes this
+// lane's 4*(l/32)), via two LDS transpose loads.  Within a 16-lane group,
+// lane c addresses row (c>>2), columns 4*(c&3)..+3 of its group's 16-column
+// slab; the transpose hands lane i the column slab+i of the four rows.
+__device__ __forceinline__ bf16x8 read_tr(const u16 *lds, int stride, int krow,
+                                          int ncol, int lane) {
+  const int c = lane & 15;
+  const u16 *p = lds + (krow + (c >> 2)) * stride + ncol + ((lane >> 4) & 1) * 16 + 4 * (c & 3);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p + 8 * stride));
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  const v8i16 x = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, x);
+}
+
+template <int D>
+struct StreamSmem {
+  union {
+    struct {
+      u16 a[TILE * (D + RM_PAD)];
+      u16 b[TILE * (D + RM_PAD)];
+    } t;
+    float red[2][32 * D];                // cross-wave sums at the end of an item
+  };
+  alignas(16) float pos[4 * POS_COPY];
+  alignas(16) int32_t ts32[TILE];        // streamed-tile timestamps - ts_start
+  int64_t ts64[TILE];                    // raw streamed-tile timestamps
+  int flag[2];                           // "some timestamp is far" (parity-buffered)
+  int item;
+};
+
+// Per-lane running sum of d_time contributions over one time index (the
+// lane's pairs visit non-decreasing indices when timestamps are ordered, so
+// a run is flushed only when its index changes).
+struct TimeRun {
+  float sum = 0.0f;
+  int cur = -1;
+  __device__ __forceinline__ void add(fix64 *acc, int k, float v) {
+    if (k != cur) {
+      if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
+      cur = k;
+      sum = 0.0f;
+    }
+    sum += v;
+  }
+  __device__ __forceinline__ void flush(fix64 *acc) {
+    if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
+    cur = -1;
+    sum = 0.0f;
+  }
+};
+
+
+// Integer time difference -> float-exponent index (|delta| < 2^24).
+__device__ __forceinline__ int time_index(int32_t delta) {
+  return (int)__builtin_amdgcn_ubfe(__float_as_uint((float)delta), 21u, 10u);
+}
+
+// silu'(x) / N = sigma(x) (1 + x (1 - sigma(x))) / N
+__device__ __forceinline__ float dsilu_over_n(float x, float inv_n) {
+  const float sg = sigmoid_f(x);
+  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * inv_n;
+}
+
 // --------------------------------------------------------------------- dQ
 // One q-stationary item: dQ_i = sum_{j<=i} dS_ij k_j for a 64-row query tile
 // of one head, recomputing S and dA = dO V^T tile by tile.
@@ -663,16 +682,16 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     load_stationary<D>(P.dO + qoff, i_loc, q_valid, row_stride, g, doreg);
 
     int64_t ts_start = 0, ts_i = 0;
-    float ts_i32 = 0.0f;
+    int32_t ts_i32 = 0;
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
-      ts_i32 = (float)(int32_t)rel;
+      ts_i32 = (int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid, 1.0f);
     }
 
     f32x16 acc[D / 32];
@@ -688,7 +707,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
       vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
       if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
-      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid);
+      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid, 1.0f);
     }
 
     for (int kt = 0; kt <= qt; ++kt, ++phase) {
@@ -700,7 +719,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
-          sm.ts32[tid] = (float)(int32_t)rel;
+          sm.ts32[tid] = (int32_t)rel;
           sm.ts64[tid] = ts_k;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -715,7 +734,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
       }
 
       f32x16 s, da;
@@ -728,26 +747,23 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       }
 
       float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = s[r];
       const int kb = 32 * wj + 4 * g;
       if (POS) {
         const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pb.x);
-          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pb.y);
-          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pb.z);
-          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pb.w);
+          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
+          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
         }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
       }
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const float4 t4 = *(const float4 *)(sm.ts32 + kb + 8 * q4);
+            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
             x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
             x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
             x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
@@ -759,14 +775,9 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
             x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
       }
-      // dS N = dA silu'(x) = dA (sg + x sg (1 - sg)); the 1/N goes on dQ
       float dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float sg = sigmoid2(x[r]);
-        const float u = (x[r] * LN2) * sg;
-        dsv[r] = da[r] * __builtin_fmaf(u, 1.0f - sg, sg);
-      }
+      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu_over_n(x[r], P.inv_n);
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -789,7 +800,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     }
 
     sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
-                      row_stride, q_valid, P.inv_n);
+                      row_stride, q_valid, 1.0f);
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -842,16 +853,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
 
     int64_t ts_start = 0, ts_j = 0;
-    float ts_j32 = 0.0f;
+    int32_t ts_j32 = 0;
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
       ts_start = P.ts[si.start];
       ts_j = j_loc < k_valid ? P.ts[si.start + (int64_t)kt * TILE + j_loc] : ts_start;
       const int64_t rel = ts_j - ts_start;
-      ts_j32 = (float)(int32_t)rel;
+      ts_j32 = (int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid);
+      ktab = item_time_slot(P, dyn, h, tid, 1.0f);
     }
     TimeRun run;                              // fast path: by float-exponent index
     fix64 *my_t = TIME ? tacc + h * P.nb : nullptr;
@@ -864,7 +875,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
 
     TileRegs<D> qr, dr;
     int64_t ts_q = 0;
-    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid) : 0.0f;
+    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, 1.0f) : 0.0f;
     {
       const int64_t r0 = si.start + (int64_t)kt * TILE;
       qr.load(P.q + (r0 * P.H + h) * D, k_valid, row_stride, tid);
@@ -873,7 +884,6 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     }
 
     for (int qt = kt; qt < si.ntiles; ++qt, ++phase) {
-      const int q_valid = si.len - qt * TILE;
       lds_barrier();
       qr.store(sm.t.a, tid);
       dr.store(sm.t.b, tid);
@@ -886,7 +896,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         bool far = k_far;
         if (tid < TILE) {
           const int64_t rel = ts_q - ts_start;
-          sm.ts32[tid] = (float)(int32_t)rel;
+          sm.ts32[tid] = (int32_t)rel;
           sm.ts64[tid] = ts_q;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -901,7 +911,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
         dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
         if (TIME && tid < TILE) ts_q = tid < nv ? P.ts[r0 + tid] : ts_start;
-        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid);
+        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, 1.0f);
       }
 
       // S and dA quadrants [32 queries x 32 keys]; lane holds key j_loc
@@ -920,26 +930,23 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       const int ib = 32 * wi + 4 * g;
       const int x0 = j_loc - ib + (TILE - 1);
       float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = s[r];
       if (POS) {
         const float *pl = pos_lane(sm.pos, 2 * TILE - 2 - x0);
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pb.x);
-          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pb.y);
-          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pb.z);
-          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pb.w);
+          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
+          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
         }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
       }
       int tk[16];
       if (TIME) {
         if (!slow) {
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const float4 t4 = *(const float4 *)(sm.ts32 + ib + 8 * q4);
+            const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * q4);
             tk[4 * q4 + 0] = time_index(t4.x - ts_j32);
             tk[4 * q4 + 1] = time_index(t4.y - ts_j32);
             tk[4 * q4 + 2] = time_index(t4.z - ts_j32);
@@ -955,18 +962,17 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
           }
         }
       }
-      // N a = silu(x) = x sg, N dS = dA silu'(x) = dA (sg + a1 (1 - sg))
-      // with a1 = x sg; the 1/N goes on dK, dV and the tables at the end.
-      // Query rows past the sequence have dO = 0, hence dA = 0 and dS = 0,
-      // and contribute a * 0 to dV: only the diagonal tile needs a mask
-      // (the causal one).
+      // a = silu(x)/N, dS = dA silu'(x)/N = dA (sg + a' (1 - sg))/N with
+      // a' = x sg.  Query rows past the sequence have dO = 0, hence dA = 0
+      // and dS = 0, and contribute a * 0 to dV: only the diagonal tile
+      // needs a mask (the causal one).
       float av[16], dsv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float sg = sigmoid2(x[r]);
-        const float a1 = (x[r] * LN2) * sg;
-        av[r] = a1;
-        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1);
+        const float sg = sigmoid_f(x[r]);
+        const float a1 = x[r] * sg;
+        av[r] = a1 * P.inv_n;
+        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1) * P.inv_n;
       }
       if (qt == kt) {
 #pragma unroll
@@ -1062,9 +1068,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
-                      row_stride, k_valid, P.inv_n);
+                      row_stride, k_valid, 1.0f);
     sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
-                      row_stride, k_valid, P.inv_n);
+                      row_stride, k_valid, 1.0f);
 }
 
 // Backward: one persistent launch over the combined list, whose entries are
@@ -1086,7 +1092,7 @@ attn_bwd_kernel(KParams P) {
   if (TIME) {
     for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
     for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0;
-    stage_all_heads(P, dyn, tid0);
+    stage_all_heads(P, dyn, tid0, 1.0f);
   }
   if (tid0 < 2) sm.flag[tid0] = 0;
   if (POS) {
