@@ -143,23 +143,9 @@ __device__ __forceinline__ float silu2_over_n(float xs, float nl) {
   return xs * __builtin_amdgcn_rcpf(__builtin_fmaf(nl, t, nl));
 }
 
-// d_time is accumulated in LDS as 64-bit fixed point (value * 2^24) with
-// integer atomics: LDS float atomics cost hundreds of cycles per wave
-// instruction here, integer ones do not.  Range: each added run sum below
-// 2^31 in magnitude and each work-group partial below 2^39; resolution
-// 2^-24 (6e-8) per added run.
-typedef unsigned long long fix64;
-
-__device__ __forceinline__ fix64 to_fixed(float v) {
-  const float fl = __builtin_floorf(v);
-  const int hi = (int)fl;                                   // saturating cvt
-  const unsigned lo = (unsigned)((v - fl) * 16777216.0f);   // [0, 2^24]
-  return (fix64)(((long long)hi << 24) + (long long)lo);
-}
-
-__device__ __forceinline__ float from_fixed(fix64 v) {
-  return (float)((double)(long long)v * (1.0 / 16777216.0));
-}
+// d_time is accumulated in LDS in double precision: the gfx950 LDS f64 add
+// atomic runs at a few cycles per wave instruction on distinct addresses,
+// while the f32 one costs hundreds.
 
 
 
@@ -624,20 +610,21 @@ struct StreamSmem {
 
 // Per-lane running sum of d_time contributions over one time index (the
 // lane's pairs visit non-decreasing indices when timestamps are ordered, so
-// a run is flushed only when its index changes).
+// a run is flushed only when its index changes).  A run is opened by the
+// first index of the item's first tile (start), so adding needs no test for
+// an empty run.
 struct TimeRun {
   float sum = 0.0f;
   int cur = -1;
-  __device__ __forceinline__ void add(fix64 *acc, int k, float v) {
-    if (k != cur) {
-      if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
-      cur = k;
-      sum = 0.0f;
-    }
-    sum += v;
+  __device__ __forceinline__ void start(int k) { cur = cur < 0 ? k : cur; }
+  __device__ __forceinline__ void add(double *acc, int k, float v) {
+    const bool change = k != cur;
+    if (change) atomicAdd(&acc[cur], (double)sum);
+    sum = change ? v : sum + v;
+    cur = k;
   }
-  __device__ __forceinline__ void flush(fix64 *acc) {
-    if (cur >= 0) atomicAdd(&acc[cur], to_fixed(sum));
+  __device__ __forceinline__ void flush(double *acc) {
+    if (cur >= 0) atomicAdd(&acc[cur], (double)sum);
     cur = -1;
     sum = 0.0f;
   }
@@ -804,32 +791,50 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
 }
 
 // ------------------------------------------------------------------ dK/dV
-// d_pos of a tile pair without LDS atomics (which cost hundreds of cycles
-// per instruction here): every lane stores its dS values "sheared" -- row
-// i, column j - i + 63 -- so that each diagonal becomes one column, and the
-// columns are then summed with plain loads.  The odd row stride keeps both
-// the stores (fixed i, consecutive j) and the column reads bank-conflict free.
-constexpr int SHEAR_STRIDE = 2 * TILE + 9;
-
+// d_pos of a k-stationary item by diagonal, summed in LDS double windows
+// with the LDS f64 add atomic.  Slot x of the window of tile pair (qt, kt)
+// holds diagonal m = i - j = (qt - kt)*64 + x - 63, i.e. x = i_loc - j_loc
+// + 63, so a lane's 16 elements sit at fixed offsets from one address; one
+// copy per lane group g keeps the 64 lanes of each atomic on distinct
+// slots.  Tile pairs alternate between two windows.  Once the next tile
+// pair's first barrier has passed, slots x < 64 of the previous window are
+// final (no later tile pair reaches those diagonals) and go to the
+// sequence's global partial, slots x >= 64 carry into slot x - 64 of the
+// current window, and the previous window is cleared for reuse.
 template <int D, bool POS>
 struct DkvSmem {
   StreamSmem<D> s;
-  float shear[POS ? TILE * SHEAR_STRIDE : 1];
-  // d_pos of the current item by diagonal m = i - j, rolling over 128 slots
-  // (m & 127): a tile pair touches 127 consecutive diagonals, the next one
-  // shifts them by 64, so only completed diagonals leave for global memory.
-  // Two windows: the upper and lower 32 rows of the tile are summed by
-  // different threads, each keeping (and flushing) its own window.
-  float dwin[POS ? 2 * 2 * TILE : 1];
-  fix64 kacc[KTAB];             // this item's d_time by float-exponent index
+  double pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
+  double kacc[KTAB];            // this item's d_time by float-exponent index
 };
+
+// Slot x (< 127) of the finished window `prev` of tile offset dt = qt - kt:
+// the two copies are summed and cleared; a final diagonal m is returned
+// through (dst, val) for a deferred global atomic into dp[m * H] (dp: this
+// sequence's and head's partials), a carried one is added into `cur`.
+__device__ __forceinline__ void dpos_retire(double (*prev)[2 * TILE], double (*cur)[2 * TILE],
+                                            int x, int dt, bool last, int len, float *dp,
+                                            int H, float *&dst, float &val) {
+  const double v = prev[0][x] + prev[1][x];
+  prev[0][x] = 0.0;
+  prev[1][x] = 0.0;
+  if (x < TILE || last) {
+    const int m = dt * TILE + x - (TILE - 1);
+    if (v != 0.0 && m >= 0 && m < len) {
+      dst = dp + m * H;
+      val = (float)v;
+    }
+  } else if (v != 0.0) {
+    atomicAdd(&cur[0][x - TILE], v);
+  }
+}
 
 // One k-stationary item: dV_j, dK_j for a 64-row key tile of one head over
 // its query tiles, with the table gradients (d_pos through the sheared tile
 // and the rolling diagonal window, d_time through per-lane index runs).
 template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx, float *dyn,
-                                         fix64 *tacc, const int tid0, const WorkEntry e,
+                                         double *tacc, const int tid0, const WorkEntry e,
                                          const int h, int &phase, float *&pend_p,
                                          float &pend_v) {
   constexpr int ST = D + RM_PAD;
@@ -865,7 +870,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       ktab = item_time_slot(P, dyn, h, tid, 1.0f);
     }
     TimeRun run;                              // fast path: by float-exponent index
-    fix64 *my_t = TIME ? tacc + h * P.nb : nullptr;
+    double *my_t = TIME ? tacc + h * P.nb : nullptr;
+    float *dp_item = POS ? P.dpos_part + si.start * P.H + h : nullptr;
 
     f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -887,10 +893,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       lds_barrier();
       qr.store(sm.t.a, tid);
       dr.store(sm.t.b, tid);
-      if (POS) {
+      if constexpr (POS) {
         pos_store<true>(pos_v, sm.pos, tid);
         if (pend_p) atomicAdd(pend_p, pend_v);
         pend_p = nullptr;
+        if (qt > kt && tid < 2 * TILE - 1) {
+          dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid, qt - 1 - kt,
+                      false, si.len, dp_item, P.H, pend_p, pend_v);
+          if (pend_p) atomicAdd(pend_p, pend_v);
+          pend_p = nullptr;
+        }
       }
       if (TIME) {
         bool far = k_far;
@@ -979,23 +991,29 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         for (int r = 0; r < 16; ++r)
           if (ib + c_row(r, 0) < j_loc) { av[r] = 0.0f; dsv[r] = 0.0f; }
       }
-      if (POS) {
-        // element (i, j) -> shear[i][j - i + 63]; i = ib + c_row(r, 0)
-        float *sh = smx.shear + ib * SHEAR_STRIDE + x0;
+      if constexpr (POS) {
+        // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0)
+        double *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sh[c_row(r, 0) * (SHEAR_STRIDE - 1)] = dsv[r];
+        for (int r = 0; r < 16; ++r) atomicAdd(pw + c_row(r, 0), (double)dsv[r]);
       }
       if (TIME) {
         // slow tiles accumulate by bucket straight into the work-group
         // histogram; fast tiles by float-exponent index, folded per item
         if (!slow) {
+          run.start(tk[0]);
 #pragma unroll
           for (int r = 0; r < 16; ++r)
             run.add(smx.kacc, tk[r], dsv[r]);
         } else {
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (dsv[r] != 0.0f) atomicAdd(&my_t[tk[r]], to_fixed(dsv[r]));
+          for (int r = 0; r < 16; ++r) {
+            // converted here, not shared with the d_pos atomics: a shared
+            // conversion would keep 16 doubles live across this branch
+            float v = dsv[r];
+            asm volatile("" : "+v"(v));
+            if (v != 0.0f) atomicAdd(&my_t[tk[r]], (double)v);
+          }
         }
       }
 
@@ -1019,50 +1037,22 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
           dk[db] = mfma32(d8, read_tr(sm.t.a, ST, krow, 32 * db, lane), dk[db]);
         }
       }
-      if (POS) {
-        // column c of the sheared tile is diagonal m = (qt-kt)*64 - (c-63);
-        // thread (c, half) sums rows 32 half .. 32 half + 31 of it
-        // (independent loads; rows outside the tile hold 0), adds that to
-        // its half's rolling window, and sends diagonals no later tile
-        // touches (c >= 63, or every one on the item's last tile) to the
-        // sequence's d_pos partial
-        lds_barrier();
-        const int c = tid & (2 * TILE - 1), half = tid >> 7;
-        if (c < 2 * TILE - 1) {
-          float v0 = 0.0f, v1 = 0.0f, v2 = 0.0f, v3 = 0.0f;
-#pragma unroll
-          for (int i = 0; i < TILE / 2; i += 4) {
-            const float *col = smx.shear + (32 * half + i) * SHEAR_STRIDE + c;
-            v0 += col[0];
-            v1 += col[SHEAR_STRIDE];
-            v2 += col[2 * SHEAR_STRIDE];
-            v3 += col[3 * SHEAR_STRIDE];
-          }
-          const int m = (qt - kt) * TILE - (c - (TILE - 1));
-          const int slot = half * 2 * TILE + (m & (2 * TILE - 1));
-          const float acc = smx.dwin[slot] + ((v0 + v1) + (v2 + v3));
-          if (c >= TILE - 1 || qt + 1 == si.ntiles) {
-            smx.dwin[slot] = 0.0f;
-            if (acc != 0.0f && m >= 0 && m < si.len) {
-              pend_p = &P.dpos_part[(si.start + m) * P.H + h];
-              pend_v = acc;
-            }
-          } else {
-            smx.dwin[slot] = acc;
-          }
-        }
-      }
     }
 
     // sum the two query halves, store dK, dV (bf16); fold this item's
     // d_time by index into the work-group histogram
     if (TIME) run.flush(smx.kacc);
     lds_barrier();
+    if constexpr (POS) {   // every diagonal of the last window is final
+      if (tid < 2 * TILE - 1)
+        dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid,
+                    si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
+    }
     if (TIME) {
       for (int x = tid; x < KTAB; x += THREADS) {
-        const fix64 val = smx.kacc[x];
-        if (val != 0) {
-          smx.kacc[x] = 0;
+        const double val = smx.kacc[x];
+        if (val != 0.0) {
+          smx.kacc[x] = 0.0;
           atomicAdd(&my_t[bucket_of_index(x, P.nb)], val);
         }
       }
@@ -1082,25 +1072,21 @@ __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_bwd_kernel(KParams P) {
   __shared__ DkvSmem<D, POS> smx;
   StreamSmem<D> &sm = smx.s;
-  // dynamic LDS: [H][nb] d_time (fixed point), then the time tables
-  extern __shared__ fix64 dyn_k[];
-  fix64 *tacc = dyn_k;
+  // dynamic LDS: [H][nb] d_time (double), then the time tables
+  extern __shared__ double dyn_k[];
+  double *tacc = dyn_k;
   float *dyn = (float *)(dyn_k + P.H * P.nb);
   const int tid0 = threadIdx.x;
   const int n_items = 2 * P.ctrl[CTRL_N_ENTRIES] * P.H;
 
   if (TIME) {
-    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
-    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0;
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
+    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0;
     stage_all_heads(P, dyn, tid0, 1.0f);
   }
   if (tid0 < 2) sm.flag[tid0] = 0;
-  if (POS) {
-    smx.dwin[tid0] = 0.0f;   // 4 TILE = THREADS slots
-    // positions (i, j - i + 63) with j outside the tile are never written
-    // again, so zero once: the column sums below read every row
-    for (int x = tid0; x < TILE * SHEAR_STRIDE; x += THREADS) smx.shear[x] = 0.0f;
-  }
+  if constexpr (POS)
+    for (int x = tid0; x < 2 * 2 * 2 * TILE; x += THREADS) (&smx.pwin[0][0][0])[x] = 0.0;
   int phase = 0;
   // A finished d_pos diagonal sum is sent one tile later, right after the
   // next wait for the prefetched tiles: the wait counter also counts
@@ -1129,7 +1115,7 @@ attn_bwd_kernel(KParams P) {
     lds_barrier();
     float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
     for (int x = tid0; x < P.H * P.nb; x += THREADS)
-      if (tacc[x] != 0) atomicAdd(&part[x], from_fixed(tacc[x]));
+      if (tacc[x] != 0.0) atomicAdd(&part[x], (float)tacc[x]);
   }
 }
 
@@ -1157,7 +1143,7 @@ size_t slots_bytes(const Problem &p) {
 }
 size_t q_dyn_bytes(const Problem &p) { return slots_bytes(p); }
 size_t k_dyn_bytes(const Problem &p) {
-  return p.has_time ? slots_bytes(p) + sizeof(unsigned long long) * (size_t)p.nb * p.H : 0;
+  return p.has_time ? slots_bytes(p) + sizeof(double) * (size_t)p.nb * p.H : 0;
 }
 
 KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
