@@ -533,8 +533,8 @@ attn_fwd_kernel(KParams P) {
 // The backward kernel stages its streamed tiles through registers into a
 // padded row-major LDS tile (measured faster here than the forward's
 // DMA-filled buffers: the backward is register-bound and the staging
-// overlaps with its longer tile step) and works in natural units with
-// 1/N applied per element.
+// overlaps with its longer tile step) and works in natural units on N A and
+// N dS, with 1/N applied to the accumulated results.
 
 // A 64-row tile of one head, D bf16 per row, moved global -> registers ->
 // LDS in 16-byte chunks; rows at or beyond `valid` are zeros, so padded
@@ -636,10 +636,13 @@ __device__ __forceinline__ int time_index(int32_t delta) {
   return (int)__builtin_amdgcn_ubfe(__float_as_uint((float)delta), 21u, 10u);
 }
 
-// silu'(x) / N = sigma(x) (1 + x (1 - sigma(x))) / N
-__device__ __forceinline__ float dsilu_over_n(float x, float inv_n) {
+// silu'(x) = sigma(x) (1 + x (1 - sigma(x))).  The backward kernels work
+// with N dS and N A (the 1/N of both is applied once, to the accumulated
+// dQ, dK, dV tiles at their store and to the table gradients when they are
+// finalized).
+__device__ __forceinline__ float dsilu(float x) {
   const float sg = sigmoid_f(x);
-  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f) * inv_n;
+  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f);
 }
 
 // --------------------------------------------------------------------- dQ
@@ -764,7 +767,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       }
       float dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu_over_n(x[r], P.inv_n);
+      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu(x[r]);
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -787,7 +790,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     }
 
     sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
-                      row_stride, q_valid, 1.0f);
+                      row_stride, q_valid, P.inv_n);
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -983,8 +986,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       for (int r = 0; r < 16; ++r) {
         const float sg = sigmoid_f(x[r]);
         const float a1 = x[r] * sg;
-        av[r] = a1 * P.inv_n;
-        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1) * P.inv_n;
+        av[r] = a1;
+        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1);
       }
       if (qt == kt) {
 #pragma unroll
@@ -1058,9 +1061,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
-                      row_stride, k_valid, 1.0f);
+                      row_stride, k_valid, P.inv_n);
     sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
-                      row_stride, k_valid, 1.0f);
+                      row_stride, k_valid, P.inv_n);
 }
 
 // Backward: one persistent launch over the combined list, whose entries are

@@ -167,8 +167,8 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 //     work-groups folded theirs into.  Block = 64 consecutive (h, k)
 //     columns; waves stride over the bins.
 // Summation order is fixed, so the result is deterministic given the
-// partials.  `scale` multiplies every entry (1: the backward kernel
-// accumulates dS itself).
+// partials.  `scale` multiplies every entry (1/N: the backward kernel
+// accumulates N dS).
 constexpr int FIN_THREADS = 1024;
 constexpr int FIN_WAVES = FIN_THREADS / 64;
 
@@ -274,7 +274,7 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                      d_pos ? (const float *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
                      d_pos, pos_blocks,
                      d_time ? (const float *)(ws + a.L.dtime_part) : nullptr,
-                     DTIME_BINS, width, d_time, 1.0f);
+                     DTIME_BINS, width, d_time, 1.0f / (float)p.N);
   return hipGetLastError();
 }
 
