@@ -183,7 +183,14 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   L.list_b = for_bwd ? take(2 * sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
   L.dO = for_bwd ? take(elem * (size_t)p.T * p.H * p.d) : 0;
   const bool bf16_bwd = for_bwd && p.dtype == HSTU_BF16;
-  L.bwd_grid = bf16_bwd ? attn_bwd_grid(p, dev) : 0;
+  L.bwd_grid_both = bf16_bwd ? attn_bwd_grid(p, dev) : 0;
+  L.bwd_grid_dq = bf16_bwd ? attn_bwd_dq_grid(p, dev) : 0;
+  L.bwd_grid_dkv = bf16_bwd ? attn_bwd_dkv_grid(p, dev) : 0;
+  // Few items per work-group (short sequences): one launch over both item
+  // kinds balances better than two launches with a tail each.  Otherwise
+  // each kind runs at its own occupancy.
+  L.bwd_combined = bf16_bwd && p.max_entries * p.H < (int64_t)BWD_COMBINED_ITEMS_PER_WG *
+                                                      std::max(L.bwd_grid_both, 1);
   L.dpos_part = (bf16_bwd && p.has_pos) ? take(sizeof(float) * (size_t)p.T * p.H) : 0;
   L.dtime_part = (bf16_bwd && p.has_time)
                      ? take(sizeof(float) * (size_t)DTIME_BINS * p.H * p.nb)
@@ -341,10 +348,7 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
     if (e != hipSuccess) return hip_fail(e, "schedule launch");
   }
   if (p.dtype == HSTU_BF16) {
-    {
-      prof::Scope ps("attn_bwd", s);
-      e = launch_attn_bwd_bf16(a, ws + L.dO, io->dq, io->dk, io->dv, s);
-    }
+    e = launch_attn_bwd_bf16(a, ws + L.dO, io->dq, io->dk, io->dv, s);
     if (e != hipSuccess) return hip_fail(e, "attention backward launch");
     {
       prof::Scope ps("finalize_tables", s);

@@ -6,12 +6,17 @@
 // scheduler's longest-first lists:
 //
 //   attn_fwd   q-stationary: O_i = sum_{j<=i} silu(s_ij)/N v_j
-//   attn_bwd   one launch over two item kinds:
-//              dQ items, q-stationary: dQ_i = sum_{j<=i} dS_ij k_j
-//              dK/dV items, k-stationary: dV_j = sum_{i>=j} a_ij dO_i,
-//                dK_j = sum_{i>=j} dS_ij q_i, plus the table gradients
-//                (per-sequence diagonal partials for d_pos, binned
-//                per-work-group histograms for d_time)
+//   attn_bwd_dkv  k-stationary: dV_j = sum_{i>=j} a_ij dO_i,
+//                 dK_j = sum_{i>=j} dS_ij q_i, plus the table gradients
+//                 (per-sequence diagonal partials for d_pos, binned
+//                 per-work-group histograms for d_time)
+//   attn_bwd_dq   q-stationary: dQ_i = sum_{j<=i} dS_ij k_j
+//   attn_bwd      both item kinds in one launch (small problems)
+//
+// With many items per work-group the two backward item kinds run as two
+// launches, each at the occupancy its own register footprint allows (the dQ
+// item holds two operands and one accumulator, the dK/dV item two and two);
+// with few (short sequences), one launch over a merged list balances better.
 //
 // with s_ij = <q_i,k_j> + pos_w[h, j-i+N-1] + time_w[h, bucket(ts_i-ts_j)],
 // dS_ij = <dO_i, v_j> silu'(s_ij) / N, and the causal mask applied after the
@@ -297,11 +302,10 @@ struct FwdSmem {
                                          // by parity of the publishing item
 };
 
-// A work-list item decoded: sequence start and length, tile, head and (in
-// the backward list) the dQ flag.
+// A work-list item decoded: sequence start and length, tile, head.
 struct Item {
   int64_t start;
-  int32_t len, tile, h, dq;
+  int32_t len, tile, h;
 };
 
 __device__ __forceinline__ Item load_item(const KParams &P, int idx) {
@@ -309,8 +313,7 @@ __device__ __forceinline__ Item load_item(const KParams &P, int idx) {
   Item it;
   it.start = e.start;
   it.len = e.len;
-  it.tile = e.tile & ~BWD_DQ_FLAG;
-  it.dq = e.tile & BWD_DQ_FLAG;
+  it.tile = e.tile;
   it.h = idx % P.H;
   return it;
 }
@@ -765,9 +768,18 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
             x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
       }
-      float dsv[16];
+      // silu'(x) dA, stage by stage over the 16 elements (independent chains
+      // side by side instead of one dependent chain per element)
+      float sg[16], dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dsv[r] = da[r] * dsilu(x[r]);
+      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_exp2f(x[r] * -L2E);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_rcpf(1.0f + sg[r]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        dsv[r] = (sg[r] * da[r]) * __builtin_fmaf(x[r], 1.0f - sg[r], 1.0f);
       if (kt == qt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -981,13 +993,18 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       // a' = x sg.  Query rows past the sequence have dO = 0, hence dA = 0
       // and dS = 0, and contribute a * 0 to dV: only the diagonal tile
       // needs a mask (the causal one).
-      float av[16], dsv[16];
+      float av[16], dsv[16], sg[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_exp2f(x[r] * -L2E);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_rcpf(1.0f + sg[r]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float sg = sigmoid_f(x[r]);
-        const float a1 = x[r] * sg;
+        const float a1 = x[r] * sg[r];
         av[r] = a1;
-        dsv[r] = da[r] * __builtin_fmaf(-a1, sg, sg + a1);
+        dsv[r] = da[r] * __builtin_fmaf(-a1, sg[r], sg[r] + a1);
       }
       if (qt == kt) {
 #pragma unroll
@@ -1066,10 +1083,41 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
                       row_stride, k_valid, P.inv_n);
 }
 
-// Backward: one persistent launch over the combined list, whose entries are
-// dK/dV items (k-stationary) and dQ items (flagged, q-stationary) in one
-// longest-first order, so the two item kinds overlap instead of running as
-// two launches back to back.
+// Work-group start of the kernels that run dK/dV items: zeroed d_time
+// histogram and index accumulators, staged time tables, cleared flags and
+// d_pos windows.
+template <int D, bool POS, bool TIME>
+__device__ __forceinline__ void dkv_kernel_init(const KParams &P, DkvSmem<D, POS> &smx,
+                                                double *tacc, float *dyn, int tid0) {
+  if (TIME) {
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
+    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0;
+    stage_all_heads(P, dyn, tid0, 1.0f);
+  }
+  if (tid0 < 2) smx.s.flag[tid0] = 0;
+  if constexpr (POS)
+    for (int x = tid0; x < 2 * 2 * 2 * TILE; x += THREADS) (&smx.pwin[0][0][0])[x] = 0.0;
+}
+
+// Work-group end: the last deferred d_pos sum (a finished diagonal is sent
+// one tile later, after the next wait for the prefetched tiles, because that
+// wait also counts atomics), then this work-group's d_time histogram folded
+// into one of DTIME_BINS partials.
+template <int D, bool POS, bool TIME>
+__device__ __forceinline__ void dkv_kernel_fini(const KParams &P, double *tacc, int tid0,
+                                                float *pend_p, float pend_v) {
+  if (POS && pend_p) atomicAdd(pend_p, pend_v);
+  if (TIME) {
+    lds_barrier();
+    float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
+    for (int x = tid0; x < P.H * P.nb; x += THREADS)
+      if (tacc[x] != 0.0) atomicAdd(&part[x], (float)tacc[x]);
+  }
+}
+
+// Backward, both item kinds in one launch over the combined list, whose
+// entries are dK/dV items (k-stationary) and dQ items (flagged,
+// q-stationary) in one longest-first order.
 template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_bwd_kernel(KParams P) {
@@ -1081,23 +1129,10 @@ attn_bwd_kernel(KParams P) {
   float *dyn = (float *)(dyn_k + P.H * P.nb);
   const int tid0 = threadIdx.x;
   const int n_items = 2 * P.ctrl[CTRL_N_ENTRIES] * P.H;
-
-  if (TIME) {
-    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
-    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0;
-    stage_all_heads(P, dyn, tid0, 1.0f);
-  }
-  if (tid0 < 2) sm.flag[tid0] = 0;
-  if constexpr (POS)
-    for (int x = tid0; x < 2 * 2 * 2 * TILE; x += THREADS) (&smx.pwin[0][0][0])[x] = 0.0;
+  dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
   int phase = 0;
-  // A finished d_pos diagonal sum is sent one tile later, right after the
-  // next wait for the prefetched tiles: the wait counter also counts
-  // atomics, so sending it at the end of its own tile would put a full
-  // atomic round trip into every iteration.
   float *pend_p = nullptr;
   float pend_v = 0.0f;
-
   for (;;) {
     if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
     lds_barrier();
@@ -1112,14 +1147,54 @@ attn_bwd_kernel(KParams P) {
       dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v);
     }
   }
-  if (POS && pend_p) atomicAdd(pend_p, pend_v);
-  if (TIME) {
-    // fold this work-group's histogram into one of DTIME_BINS partials
+  dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
+}
+
+// Backward, dQ: persistent work-groups pop q-tile items longest first.
+template <int D, bool POS, bool TIME>
+__global__ void __launch_bounds__(THREADS, D == 64 ? (TIME ? 2 : 3) : 2)
+attn_bwd_dq_kernel(KParams P) {
+  __shared__ StreamSmem<D> sm;
+  extern __shared__ float dyn_q[];            // time tables
+  const int tid0 = threadIdx.x;
+  const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
+  if (TIME) stage_all_heads(P, dyn_q, tid0, 1.0f);
+  if (tid0 < 2) sm.flag[tid0] = 0;
+  int phase = 0;
+  for (;;) {
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
     lds_barrier();
-    float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
-    for (int x = tid0; x < P.H * P.nb; x += THREADS)
-      if (tacc[x] != 0.0) atomicAdd(&part[x], (float)tacc[x]);
+    const int item = sm.item;
+    if (item >= n_items) break;
+    dq_item<D, POS, TIME>(P, sm, dyn_q, tid0, P.list[item / P.H], item % P.H, phase);
   }
+}
+
+// Backward, dK/dV and the table gradients: persistent work-groups pop k-tile
+// items longest first.
+template <int D, bool POS, bool TIME>
+__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
+attn_bwd_dkv_kernel(KParams P) {
+  __shared__ DkvSmem<D, POS> smx;
+  StreamSmem<D> &sm = smx.s;
+  extern __shared__ double dyn_k[];
+  double *tacc = dyn_k;
+  float *dyn = (float *)(dyn_k + P.H * P.nb);
+  const int tid0 = threadIdx.x;
+  const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
+  dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
+  int phase = 0;
+  float *pend_p = nullptr;
+  float pend_v = 0.0f;
+  for (;;) {
+    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
+    lds_barrier();
+    const int item = sm.item;
+    if (item >= n_items) break;
+    dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, P.list[item / P.H], item % P.H, phase,
+                           pend_p, pend_v);
+  }
+  dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
 }
 
 // ------------------------------------------------------------- launchers
@@ -1208,6 +1283,20 @@ int attn_bwd_grid(const Problem &p, int dev) {
   return grid;
 }
 
+int attn_bwd_dq_grid(const Problem &p, int dev) {
+  int grid = 1;
+  HSTU_DISPATCH(attn_bwd_dq_kernel, p.d, p.has_pos, p.has_time,
+                grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
+  return grid;
+}
+
+int attn_bwd_dkv_grid(const Problem &p, int dev) {
+  int grid = 1;
+  HSTU_DISPATCH(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time,
+                grid = persistent_grid(kfn, k_dyn_bytes(p), p.max_entries * p.H, dev));
+  return grid;
+}
+
 hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
   const char *ws = (const char *)a.ws;
   KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_FWD,
@@ -1223,18 +1312,45 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
 hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
                                 void *dv, hipStream_t s) {
   const char *ws = (const char *)a.ws;
-  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_BWD,
-                          (const WorkEntry *)(ws + a.L.list_b));
-  P.dO = (const u16 *)dO;
-  P.out0 = (u16 *)dk;
-  P.out1 = (u16 *)dv;
-  P.dq_out = (u16 *)dq;
-  P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
-  P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
   const Problem &p = a.p;
-  const int grid = a.L.bwd_grid;
-  HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), k_dyn_bytes(p), s, P));
+  if (a.L.bwd_combined) {
+    prof::Scope ps("attn_bwd", s);
+    KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_BWD,
+                            (const WorkEntry *)(ws + a.L.list_b));
+    P.dO = (const u16 *)dO;
+    P.out0 = (u16 *)dk;
+    P.out1 = (u16 *)dv;
+    P.dq_out = (u16 *)dq;
+    P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
+    P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
+    HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
+                  hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_both), dim3(THREADS),
+                                     k_dyn_bytes(p), s, P));
+    return hipGetLastError();
+  }
+  {
+    prof::Scope ps("attn_bwd_dkv", s);
+    KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DKV,
+                            (const WorkEntry *)(ws + a.L.list_k));
+    P.dO = (const u16 *)dO;
+    P.out0 = (u16 *)dk;
+    P.out1 = (u16 *)dv;
+    P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
+    P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
+    HSTU_DISPATCH(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time,
+                  hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_dkv), dim3(THREADS),
+                                     k_dyn_bytes(p), s, P));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  prof::Scope ps("attn_bwd_dq", s);
+  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DQ,
+                          (const WorkEntry *)(ws + a.L.list_q));
+  P.dO = (const u16 *)dO;
+  P.dq_out = (u16 *)dq;
+  HSTU_DISPATCH(attn_bwd_dq_kernel, p.d, p.has_pos, p.has_time,
+                hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_dq), dim3(THREADS), q_dyn_bytes(p),
+                                   s, P));
   return hipGetLastError();
 }
 

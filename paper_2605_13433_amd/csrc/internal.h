@@ -19,13 +19,17 @@ constexpr int TILE = 64;
 // kernel sums the bins in a fixed order.
 constexpr int DTIME_BINS = 16;
 
+// The backward runs as one combined launch while the work list holds fewer
+// than this many (entry, head) items per persistent work-group.
+constexpr int BWD_COMBINED_ITEMS_PER_WG = 4;
+
 // Control block at the head of every workspace (int32 words).
 enum CtrlSlot {
   CTRL_N_ENTRIES = 0,   // (sequence, tile) entries in each work list
   CTRL_POP_FWD = 1,     // pop counter of the attention forward kernel
   CTRL_POP_DQ = 2,      // pop counter of the dQ kernel
-  CTRL_POP_DKV = 3,     // pop counter of the fp32 dK/dV pass
-  CTRL_POP_BWD = 4,     // pop counter of the bf16 backward kernel
+  CTRL_POP_DKV = 3,     // pop counter of the dK/dV kernel (and fp32 pass)
+  CTRL_POP_BWD = 4,     // pop counter of the combined bf16 backward kernel
   CTRL_WORDS = 64
 };
 
@@ -65,7 +69,10 @@ struct Problem {
 // 256-byte aligned.  Regions with size 0 are absent.
 struct Layout {
   size_t ctrl, seqinfo, list_q, list_k, list_b, dO, dpos_part, dtime_part, total;
-  int bwd_grid;          // persistent grid of the bf16 backward kernel (WG count)
+  // persistent grids of the bf16 backward kernels (combined, dQ, dK/dV) and
+  // whether the combined one runs (small problems) or the other two
+  int bwd_grid_both, bwd_grid_dq, bwd_grid_dkv;
+  bool bwd_combined;
 };
 
 // ---- host helpers shared by the C-ABI translation units ----
@@ -104,6 +111,7 @@ const DeviceInfo &device_info(int dev);
 
 Layout make_layout(const Problem &p, bool for_bwd, int dev);
 
+
 // ---- launchers (each returns hipSuccess or the launch error) ----
 // Builds the work lists (and zeroes the d_time bins when the layout has
 // them, so the backward's later kernels can accumulate into them).
@@ -120,7 +128,8 @@ struct AttnArgs {
 };
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s);
-// dQ, dK, dV and the table-gradient partials in one launch.
+// dQ, dK, dV and the table-gradient partials: one combined launch, or a
+// dK/dV launch then a dQ launch (see Layout::bwd_combined).
 hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
                                 void *dv, hipStream_t s);
 
@@ -154,5 +163,7 @@ hipError_t launch_zero(void *p, size_t bytes, int dev, hipStream_t s);
 // Persistent-grid sizes (work-groups) of the bf16 attention kernels.
 int attn_fwd_grid(const Problem &p, int dev);
 int attn_bwd_grid(const Problem &p, int dev);
+int attn_bwd_dq_grid(const Problem &p, int dev);
+int attn_bwd_dkv_grid(const Problem &p, int dev);
 
 }  // namespace hstu

@@ -11,11 +11,11 @@
 //
 //   * q-list: entries (b, qt) for every 64-row query tile of every sequence,
 //     cost qt+1 k-tiles (causal: only kt <= qt is visited), sorted by cost
-//     descending.  Consumed by the forward kernels and the fp32 dQ pass.
+//     descending.  Consumed by the forward kernels and the dQ kernels.
 //   * k-list: entries (b, kt), cost ntiles_b - kt q-tiles, same order rule.
-//     Consumed by the fp32 dK/dV pass.
+//     Consumed by the dK/dV kernels.
 //   * combined backward list: both kinds merged bin by bin (dQ entries
-//     flagged), consumed by the bf16 backward kernel.
+//     flagged), consumed by the combined bf16 backward kernel.
 //
 // Built on the device from seq_offsets (no host round trip) by one
 // work-group: a histogram of tile counts, a descending exclusive scan of the
