@@ -730,73 +730,71 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
       }
 
+      // S^T quadrant with the position bias as the accumulator's initial
+      // value, and dA^T
+      const int kb = 32 * wj + 4 * g;
       f32x16 s, da;
 #pragma unroll
       for (int r = 0; r < 16; ++r) { s[r] = 0.0f; da[r] = 0.0f; }
+      if (POS) {
+        const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pb = *(const float4 *)(pl + 8 * q4);
+          s[4 * q4 + 0] = pb.x; s[4 * q4 + 1] = pb.y;
+          s[4 * q4 + 2] = pb.z; s[4 * q4 + 3] = pb.w;
+        }
+      }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         s = mfma32(read_rm(sm.t.a, ST, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
         da = mfma32(read_rm(sm.t.b, ST, 32 * wj + l32, 16 * ks + 8 * g), doreg[ks], da);
       }
 
-      float x[16];
+      // dS = dA silu'(x), then dQ += dS K, one 16-key half at a time (half the
+      // temporaries live at once)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = s[r];
-      const int kb = 32 * wj + 4 * g;
-      if (POS) {
-        const float *pl = pos_lane(sm.pos, kb - i_loc + (TILE - 1));
+      for (int hh = 0; hh < 2; ++hh) {
+        float x[8], sg[8], dsv[8];
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
-          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
-        }
-      }
-      if (TIME) {
-        if (!slow) {
+        for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e];
+        if (TIME) {
+          if (!slow) {
 #pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * q4);
-            x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
-            x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
-            x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
-            x[4 * q4 + 3] += ktab[time_index(ts_i32 - t4.w)];
+            for (int q = 0; q < 2; ++q) {
+              const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * (2 * hh + q));
+              x[4 * q + 0] += ktab[time_index(ts_i32 - t4.x)];
+              x[4 * q + 1] += ktab[time_index(ts_i32 - t4.y)];
+              x[4 * q + 2] += ktab[time_index(ts_i32 - t4.z)];
+              x[4 * q + 3] += ktab[time_index(ts_i32 - t4.w)];
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              x[e] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(8 * hh + e, 0)], P.nb)];
           }
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            x[r] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(r, 0)], P.nb)];
         }
-      }
-      // silu'(x) dA, stage by stage over the 16 elements (independent chains
-      // side by side instead of one dependent chain per element)
-      float sg[16], dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_exp2f(x[r] * -L2E);
-      __builtin_amdgcn_sched_barrier(0);
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * -L2E);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_rcpf(1.0f + sg[r]);
-      __builtin_amdgcn_sched_barrier(0);
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_rcpf(1.0f + sg[e]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        dsv[r] = (sg[r] * da[r]) * __builtin_fmaf(x[r], 1.0f - sg[r], 1.0f);
-      if (kt == qt) {
+        for (int e = 0; e < 8; ++e)
+          dsv[e] = (sg[e] * da[8 * hh + e]) * __builtin_fmaf(x[e], 1.0f - sg[e], 1.0f);
+        if (kt == qt) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kb + c_row(r, 0) > i_loc) dsv[r] = 0.0f;
-      }
-
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+          for (int e = 0; e < 8; ++e)
+            if (kb + c_row(8 * hh + e, 0) > i_loc) dsv[e] = 0.0f;
+        }
         uint4 pk;
-        pk.x = pack2(dsv[8 * ks + 0], dsv[8 * ks + 1]);
-        pk.y = pack2(dsv[8 * ks + 2], dsv[8 * ks + 3]);
-        pk.z = pack2(dsv[8 * ks + 4], dsv[8 * ks + 5]);
-        pk.w = pack2(dsv[8 * ks + 6], dsv[8 * ks + 7]);
+        pk.x = pack2(dsv[0], dsv[1]);
+        pk.y = pack2(dsv[2], dsv[3]);
+        pk.z = pack2(dsv[4], dsv[5]);
+        pk.w = pack2(dsv[6], dsv[7]);
         const bf16x8 pa = as_bf16x8(pk);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          acc[db] = mfma32(pa, read_tr(sm.t.a, ST, 32 * wj + 16 * ks + 4 * g, 32 * db, lane),
+          acc[db] = mfma32(pa, read_tr(sm.t.a, ST, 32 * wj + 16 * hh + 4 * g, 32 * db, lane),
                            acc[db]);
       }
     }
@@ -941,116 +939,113 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, 1.0f);
       }
 
-      // S and dA quadrants [32 queries x 32 keys]; lane holds key j_loc
+      // this lane's queries sit at ib + 8 q4 + c, ib = 32 wi + 4 g; offset
+      // j - i = j_loc - ib - i_rel walks the slice downwards, i.e. the
+      // reversed copies upwards from 126 - x0
+      const int ib = 32 * wi + 4 * g;
+      const int x0 = j_loc - ib + (TILE - 1);
+      // S and dA quadrants [32 queries x 32 keys]; lane holds key j_loc.  The
+      // position bias is the score accumulator's initial value.
       f32x16 s, da;
 #pragma unroll
       for (int r = 0; r < 16; ++r) { s[r] = 0.0f; da[r] = 0.0f; }
+      if (POS) {
+        const float *pl = pos_lane(sm.pos, 2 * TILE - 2 - x0);
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pb = *(const float4 *)(pl + 8 * q4);
+          s[4 * q4 + 0] = pb.x; s[4 * q4 + 1] = pb.y;
+          s[4 * q4 + 2] = pb.z; s[4 * q4 + 3] = pb.w;
+        }
+      }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         s = mfma32(read_rm(sm.t.a, ST, 32 * wi + l32, 16 * ks + 8 * g), kreg[ks], s);
         da = mfma32(read_rm(sm.t.b, ST, 32 * wi + l32, 16 * ks + 8 * g), vreg[ks], da);
       }
 
-      // this lane's queries sit at ib + 8 q4 + c, ib = 32 wi + 4 g; offset
-      // j - i = j_loc - ib - i_rel walks the slice downwards, i.e. the
-      // reversed copies upwards from 126 - x0
-      const int ib = 32 * wi + 4 * g;
-      const int x0 = j_loc - ib + (TILE - 1);
-      float x[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = s[r];
-      if (POS) {
-        const float *pl = pos_lane(sm.pos, 2 * TILE - 2 - x0);
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 pb = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] += pb.x; x[4 * q4 + 1] += pb.y;
-          x[4 * q4 + 2] += pb.z; x[4 * q4 + 3] += pb.w;
-        }
-      }
-      int tk[16];
-      if (TIME) {
-        if (!slow) {
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * q4);
-            tk[4 * q4 + 0] = time_index(t4.x - ts_j32);
-            tk[4 * q4 + 1] = time_index(t4.y - ts_j32);
-            tk[4 * q4 + 2] = time_index(t4.z - ts_j32);
-            tk[4 * q4 + 3] = time_index(t4.w - ts_j32);
-          }
-#pragma unroll
-          for (int r = 0; r < 16; ++r) x[r] += ktab[tk[r]];
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            tk[r] = time_bucket(sm.ts64[ib + c_row(r, 0)] - ts_j, P.nb);
-            x[r] += ktab[KTAB + tk[r]];
-          }
-        }
-      }
       // a = silu(x)/N, dS = dA silu'(x)/N = dA (sg + a' (1 - sg))/N with
-      // a' = x sg.  Query rows past the sequence have dO = 0, hence dA = 0
-      // and dS = 0, and contribute a * 0 to dV: only the diagonal tile
-      // needs a mask (the causal one).
-      float av[16], dsv[16], sg[16];
+      // a' = x sg, the table gradients, then dV += A^T dO and dK += dS^T Q,
+      // one 16-query half at a time (half the temporaries live at once).
+      // Query rows past the sequence have dO = 0, hence dA = 0 and dS = 0,
+      // and contribute a * 0 to dV: only the diagonal tile needs a mask (the
+      // causal one).
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_exp2f(x[r] * -L2E);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int hh = 0; hh < 2; ++hh) {
+        float x[8], sg[8], av[8], dsv[8];
+        int tk[8];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sg[r] = __builtin_amdgcn_rcpf(1.0f + sg[r]);
-      __builtin_amdgcn_sched_barrier(0);
+        for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e];
+        if (TIME) {
+          if (!slow) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float a1 = x[r] * sg[r];
-        av[r] = a1;
-        dsv[r] = da[r] * __builtin_fmaf(-a1, sg[r], sg[r] + a1);
-      }
-      if (qt == kt) {
+            for (int q = 0; q < 2; ++q) {
+              const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * (2 * hh + q));
+              tk[4 * q + 0] = time_index(t4.x - ts_j32);
+              tk[4 * q + 1] = time_index(t4.y - ts_j32);
+              tk[4 * q + 2] = time_index(t4.z - ts_j32);
+              tk[4 * q + 3] = time_index(t4.w - ts_j32);
+            }
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (ib + c_row(r, 0) < j_loc) { av[r] = 0.0f; dsv[r] = 0.0f; }
-      }
-      if constexpr (POS) {
-        // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0)
-        double *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
+            for (int e = 0; e < 8; ++e) x[e] += ktab[tk[e]];
+          } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) atomicAdd(pw + c_row(r, 0), (double)dsv[r]);
-      }
-      if (TIME) {
-        // slow tiles accumulate by bucket straight into the work-group
-        // histogram; fast tiles by float-exponent index, folded per item
-        if (!slow) {
-          run.start(tk[0]);
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            run.add(smx.kacc, tk[r], dsv[r]);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            // converted here, not shared with the d_pos atomics: a shared
-            // conversion would keep 16 doubles live across this branch
-            float v = dsv[r];
-            asm volatile("" : "+v"(v));
-            if (v != 0.0f) atomicAdd(&my_t[tk[r]], (double)v);
+            for (int e = 0; e < 8; ++e) {
+              tk[e] = time_bucket(sm.ts64[ib + c_row(8 * hh + e, 0)] - ts_j, P.nb);
+              x[e] += ktab[KTAB + tk[e]];
+            }
           }
         }
-      }
-
-      // dV_wj += A^T dO, dK_wj += dS^T Q over this wave's 32 queries
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * -L2E);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_rcpf(1.0f + sg[e]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float a1 = x[e] * sg[e];
+          av[e] = a1;
+          dsv[e] = da[8 * hh + e] * __builtin_fmaf(-a1, sg[e], sg[e] + a1);
+        }
+        if (qt == kt) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (ib + c_row(8 * hh + e, 0) < j_loc) { av[e] = 0.0f; dsv[e] = 0.0f; }
+        }
+        if constexpr (POS) {
+          // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0)
+          double *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) atomicAdd(pw + c_row(8 * hh + e, 0), (double)dsv[e]);
+        }
+        if (TIME) {
+          // slow tiles accumulate by bucket straight into the work-group
+          // histogram; fast tiles by float-exponent index, folded per item
+          if (!slow) {
+            if (hh == 0) run.start(tk[0]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) run.add(smx.kacc, tk[e], dsv[e]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              // converted here, not shared with the d_pos atomics: a shared
+              // conversion would keep the doubles live across this branch
+              float v = dsv[e];
+              asm volatile("" : "+v"(v));
+              if (v != 0.0f) atomicAdd(&my_t[tk[e]], (double)v);
+            }
+          }
+        }
         uint4 pa, pd;
-        pa.x = pack2(av[8 * ks + 0], av[8 * ks + 1]);
-        pa.y = pack2(av[8 * ks + 2], av[8 * ks + 3]);
-        pa.z = pack2(av[8 * ks + 4], av[8 * ks + 5]);
-        pa.w = pack2(av[8 * ks + 6], av[8 * ks + 7]);
-        pd.x = pack2(dsv[8 * ks + 0], dsv[8 * ks + 1]);
-        pd.y = pack2(dsv[8 * ks + 2], dsv[8 * ks + 3]);
-        pd.z = pack2(dsv[8 * ks + 4], dsv[8 * ks + 5]);
-        pd.w = pack2(dsv[8 * ks + 6], dsv[8 * ks + 7]);
+        pa.x = pack2(av[0], av[1]);
+        pa.y = pack2(av[2], av[3]);
+        pa.z = pack2(av[4], av[5]);
+        pa.w = pack2(av[6], av[7]);
+        pd.x = pack2(dsv[0], dsv[1]);
+        pd.y = pack2(dsv[2], dsv[3]);
+        pd.z = pack2(dsv[4], dsv[5]);
+        pd.w = pack2(dsv[6], dsv[7]);
         const bf16x8 a8 = as_bf16x8(pa), d8 = as_bf16x8(pd);
-        const int krow = 32 * wi + 16 * ks + 4 * g;
+        const int krow = 32 * wi + 16 * hh + 4 * g;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
           dv[db] = mfma32(a8, read_tr(sm.t.b, ST, krow, 32 * db, lane), dv[db]);
