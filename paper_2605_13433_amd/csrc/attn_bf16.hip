@@ -819,6 +819,11 @@ struct DkvSmem {
   StreamSmem<D> s;
   double pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
   double kacc[KTAB];            // this item's d_time by float-exponent index
+  // At d=64 the item's stationary K and V tiles live here (swizzled, filled
+  // by global-to-LDS loads) instead of in registers, which lets the kernel
+  // run three waves per SIMD.
+  alignas(16) u16 kst[D == 64 ? TILE * D : 8];
+  alignas(16) u16 vst[D == 64 ? TILE * D : 8];
 };
 
 // Slot x (< 127) of the finished window `prev` of tile offset dt = qt - kt:
@@ -866,9 +871,19 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     const int j_loc = 32 * wj + l32;
     const int64_t koff = ((si.start + (int64_t)kt * TILE) * P.H + h) * D;
 
-    bf16x8 kreg[D / 16], vreg[D / 16];
-    load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
-    load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
+    // stationary K, V rows: registers, or (d=64) LDS tiles whose rows past
+    // the sequence repeat its last row -- those keys only occur in the last
+    // key tile's diagonal step, where the causal mask removes them, and
+    // query rows past the sequence carry dO = 0
+    constexpr bool KV_LDS = D == 64;
+    bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
+    if constexpr (KV_LDS) {
+      dma_tile<D>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
+      dma_tile<D>(P.v + koff, k_valid, row_stride, smx.vst, w, lane);
+    } else {
+      load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
+      load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
+    }
 
     int64_t ts_start = 0, ts_j = 0;
     int32_t ts_j32 = 0;
@@ -901,6 +916,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       dr.load(P.dO + (r0 * P.H + h) * D, k_valid, row_stride, tid);
       if (TIME && tid < TILE) ts_q = tid < k_valid ? P.ts[r0 + tid] : ts_start;
     }
+    if constexpr (KV_LDS) wait_vm();    // the first step's barriers publish the tiles
 
     for (int qt = kt; qt < si.ntiles; ++qt, ++phase) {
       lds_barrier();
@@ -960,8 +976,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        s = mfma32(read_rm(sm.t.a, ST, 32 * wi + l32, 16 * ks + 8 * g), kreg[ks], s);
-        da = mfma32(read_rm(sm.t.b, ST, 32 * wi + l32, 16 * ks + 8 * g), vreg[ks], da);
+        bf16x8 kop, vop;
+        if constexpr (KV_LDS) {
+          kop = sread_rm<D>(smx.kst, j_loc, 16 * ks + 8 * g);
+          vop = sread_rm<D>(smx.vst, j_loc, 16 * ks + 8 * g);
+        } else {
+          kop = kreg[ks];
+          vop = vreg[ks];
+        }
+        s = mfma32(read_rm(sm.t.a, ST, 32 * wi + l32, 16 * ks + 8 * g), kop, s);
+        da = mfma32(read_rm(sm.t.b, ST, 32 * wi + l32, 16 * ks + 8 * g), vop, da);
       }
 
       // a = silu(x)/N, dS = dA silu'(x)/N = dA (sg + a' (1 - sg))/N with
@@ -1168,7 +1192,7 @@ attn_bwd_dq_kernel(KParams P) {
 // Backward, dK/dV and the table gradients: persistent work-groups pop k-tile
 // items longest first.
 template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
+__global__ void __launch_bounds__(THREADS, D == 64 ? (TIME ? 2 : 3) : 1)
 attn_bwd_dkv_kernel(KParams P) {
   __shared__ DkvSmem<D, POS> smx;
   StreamSmem<D> &sm = smx.s;
