@@ -55,11 +55,13 @@ def kernel_work(name, w, elem_bytes):
       attn_fwd   reads q, k, v; writes o                    4 E elements
       ln_fwd     reads o, u; writes y  (+ mean, rstd)       3 E (+ 2 T fp32)
       ln_bwd     reads dy, u, o; writes du, dO (+ stats)    5 E (+ 2 T fp32)
-      attn_bwd_dkv  reads q, k, v, dO; writes dk, dv        6 E
-      attn_bwd_dq   reads q, k, v, dO; writes dq            5 E
+      attn_bwd      reads q, k, v, dO; writes dq, dk, dv    7 E   (one launch)
+      attn_bwd_dkv  reads q, k, v, dO; writes dk, dv        6 E   (or two
+      attn_bwd_dq   reads q, k, v, dO; writes dq            5 E    launches)
     Flops are the credited contractions: fwd QK^T + AV = 4 d H P; backward
-    dA, dV, dK = 6 d H P in the dK/dV kernel and dQ = 2 d H P in the dQ
-    kernel (its recomputed scores and dA are not credited).
+    dA, dQ, dV, dK = 8 d H P, of which dA, dV, dK (6 d H P) are the dK/dV
+    kernel's and dQ (2 d H P) the dQ kernel's when the backward runs as two
+    launches (the dQ kernel's recomputed scores and dA are not credited).
     """
     E = w.T * w.H * w.d
     P = w.pairs
@@ -68,6 +70,7 @@ def kernel_work(name, w, elem_bytes):
         "attn_fwd": (4 * E * elem_bytes, 4 * w.d * w.H * P),
         "ln_fwd": (3 * E * elem_bytes + tok, 0),
         "ln_bwd": (5 * E * elem_bytes + tok, 0),
+        "attn_bwd": (7 * E * elem_bytes, 8 * w.d * w.H * P),
         "attn_bwd_dkv": (6 * E * elem_bytes, 6 * w.d * w.H * P),
         "attn_bwd_dq": (5 * E * elem_bytes, 2 * w.d * w.H * P),
     }
