@@ -458,64 +458,66 @@ attn_fwd_kernel(KParams P) {
         load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
                            i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
 
-      // x' = s log2e + bias'; this lane's keys sit at 32 wj + 4 g + 8 q4 + c
-      float x[16];
+      // x' = s log2e + bias', A = silu(x)/N, then O_wi += A V, one 16-key
+      // half at a time (half the temporaries live at once); this lane's
+      // keys sit at 32 wj + 4 g + 8 q4 + c
       const int kb = 32 * wj + 4 * g;
-      if (POS) {
-        const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
+      const float nl = (float)P.N * L2E;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 pbv = *(const float4 *)(pl + 8 * q4);
-          x[4 * q4 + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pbv.x);
-          x[4 * q4 + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pbv.y);
-          x[4 * q4 + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pbv.z);
-          x[4 * q4 + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pbv.w);
-        }
-      } else {
+      for (int hh = 0; hh < 2; ++hh) {
+        float x[8];
+        if (POS) {
+          const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
 #pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] = s[r] * L2E;
-      }
-      if (TIME) {
-        if (!slow) {
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const float4 t4 = *(const float4 *)(sm.ts32[pb] + kb + 8 * q4);
-            x[4 * q4 + 0] += ktab[time_index(ts_i32 - t4.x)];
-            x[4 * q4 + 1] += ktab[time_index(ts_i32 - t4.y)];
-            x[4 * q4 + 2] += ktab[time_index(ts_i32 - t4.z)];
-            x[4 * q4 + 3] += ktab[time_index(ts_i32 - t4.w)];
+          for (int q = 0; q < 2; ++q) {
+            const int q4 = 2 * hh + q;
+            const float4 pbv = *(const float4 *)(pl + 8 * q4);
+            x[4 * q + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pbv.x);
+            x[4 * q + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pbv.y);
+            x[4 * q + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pbv.z);
+            x[4 * q + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pbv.w);
           }
         } else {
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            x[r] += ktab[KTAB + time_bucket(ts_i_item - sm.ts64[pb][kb + c_row(r, 0)], P.nb)];
+          for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e] * L2E;
         }
-      }
-      const float nl = (float)P.N * L2E;
-      float av[16];
+        if (TIME) {
+          if (!slow) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) av[r] = silu2_over_n(x[r], nl);
-      // the diagonal tile is the only one with keys past the query (and the
-      // only one that can hold rows past the sequence, repeated rows that
-      // the same mask removes)
-      if (last) {
+            for (int q = 0; q < 2; ++q) {
+              const float4 t4 = *(const float4 *)(sm.ts32[pb] + kb + 8 * (2 * hh + q));
+              x[4 * q + 0] += ktab[time_index(ts_i32 - t4.x)];
+              x[4 * q + 1] += ktab[time_index(ts_i32 - t4.y)];
+              x[4 * q + 2] += ktab[time_index(ts_i32 - t4.z)];
+              x[4 * q + 3] += ktab[time_index(ts_i32 - t4.w)];
+            }
+          } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kb + c_row(r, 0) > i_loc) av[r] = 0.0f;
-      }
-
-      // O_wi += P V over this wave's 32 keys (two 16-key k-steps)
+            for (int e = 0; e < 8; ++e)
+              x[e] += ktab[KTAB + time_bucket(ts_i_item - sm.ts64[pb][kb + c_row(8 * hh + e, 0)],
+                                              P.nb)];
+          }
+        }
+        float av[8];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+        for (int e = 0; e < 8; ++e) av[e] = silu2_over_n(x[e], nl);
+        // the diagonal tile is the only one with keys past the query (and
+        // the only one that can hold rows past the sequence, repeated rows
+        // that the same mask removes)
+        if (last) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (kb + c_row(8 * hh + e, 0) > i_loc) av[e] = 0.0f;
+        }
         uint4 pk;
-        pk.x = pack2(av[8 * ks + 0], av[8 * ks + 1]);
-        pk.y = pack2(av[8 * ks + 2], av[8 * ks + 3]);
-        pk.z = pack2(av[8 * ks + 4], av[8 * ks + 5]);
-        pk.w = pack2(av[8 * ks + 6], av[8 * ks + 7]);
+        pk.x = pack2(av[0], av[1]);
+        pk.y = pack2(av[2], av[3]);
+        pk.z = pack2(av[4], av[5]);
+        pk.w = pack2(av[6], av[7]);
         const bf16x8 pa = as_bf16x8(pk);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(pa, sread_tr<D>(vt_lds, 32 * wj + 16 * ks + 4 * g, 32 * db, lane),
+          oacc[db] = mfma32(pa, sread_tr<D>(vt_lds, 32 * wj + 16 * hh + 4 * g, 32 * db, lane),
                             oacc[db]);
       }
     }
