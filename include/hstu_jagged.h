@@ -216,11 +216,15 @@ size_t hstu_layer_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
 
 /* Runs only the seq_offsets tile scheduler (the first step of both calls)
  * and copies its work lists out, for inspection and tests.  Work is split
- * into (sequence, 64-row tile) entries; the q-list orders query tiles by
- * their causal cost (tile index + 1 key tiles), the k-list orders key tiles
- * by theirs (tiles of the sequence minus tile index), both longest first --
- * the sort-by-cost, assign-greedily balancing of Sec. 3.1.3 applied to the
- * compute units of one GPU.  Device pointers: n_entries [1] int32 receives
+ * into (sequence, 64-row tile) entries; a query tile costs its tile index
+ * + 1 key tiles (causal), a key tile the sequence's tiles minus its index.
+ * Both lists are longest first -- the sort-by-cost, assign-greedily
+ * balancing of Sec. 3.1.3 applied to the compute units of one GPU -- in one
+ * of two orders: every entry by cost, or, when the causal tile pairs reach
+ * 4 x the longest entry x 4 x (compute units), sequence by sequence
+ * (longest sequence first, each sequence's tiles longest first), which
+ * keeps concurrent work-groups on few sequences.  The choice is made on the
+ * device with one head per entry.  Device pointers: n_entries [1] int32 receives
  * the entry count E; list_q and list_k receive E int32 pairs
  * (sequence, tile) in pop order and must hold
  * min(B*ceil(max_len/64), (total_tokens + 63*B)/64) pairs.  workspace_bytes

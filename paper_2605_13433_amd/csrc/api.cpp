@@ -183,6 +183,7 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   L.list_b = for_bwd ? take(2 * sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
   L.dO = for_bwd ? take(elem * (size_t)p.T * p.H * p.d) : 0;
   const bool bf16_bwd = for_bwd && p.dtype == HSTU_BF16;
+  L.num_cu = device_info(dev).num_cu;
   L.bwd_grid_both = bf16_bwd ? attn_bwd_grid(p, dev) : 0;
   L.bwd_grid_dq = bf16_bwd ? attn_bwd_dq_grid(p, dev) : 0;
   L.bwd_grid_dkv = bf16_bwd ? attn_bwd_dkv_grid(p, dev) : 0;

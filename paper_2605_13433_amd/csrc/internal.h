@@ -73,6 +73,7 @@ struct Layout {
   // whether the combined one runs (small problems) or the other two
   int bwd_grid_both, bwd_grid_dq, bwd_grid_dkv;
   bool bwd_combined;
+  int num_cu;                         // compute units of the device
 };
 
 // ---- host helpers shared by the C-ABI translation units ----

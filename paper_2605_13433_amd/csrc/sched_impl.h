@@ -6,22 +6,34 @@
 // The paper balances jagged work by sorting samples by cost and assigning
 // them greedily (Sec. 3.1.3, "Global Token Reallocation"), and balances
 // work across the compute elements of one device (Sec. 3.1.1, step 3).  On
-// one GPU the same idea becomes a longest-processing-time-first work list
-// consumed by persistent work-groups through an atomic pop counter:
+// one GPU the same idea becomes a longest-first work list consumed by
+// persistent work-groups through an atomic pop counter (every entry expands
+// to H adjacent items, one per head):
 //
-//   * q-list: entries (b, qt) for every 64-row query tile of every sequence,
-//     cost qt+1 k-tiles (causal: only kt <= qt is visited), sorted by cost
-//     descending.  Consumed by the forward kernels and the dQ kernels.
-//   * k-list: entries (b, kt), cost ntiles_b - kt q-tiles, same order rule.
-//     Consumed by the dK/dV kernels.
-//   * combined backward list: both kinds merged bin by bin (dQ entries
-//     flagged), consumed by the combined bf16 backward kernel.
+//   * q-list: entries (b, qt) for every 64-row query tile, cost qt+1 k-tiles
+//     (causal: only kt <= qt is visited).  Consumed by the forward kernels
+//     and the dQ kernels.
+//   * k-list: entries (b, kt), cost ntiles_b - kt q-tiles.  Consumed by the
+//     dK/dV kernels.
+//   * combined backward list: both kinds, dK/dV entries before dQ entries of
+//     equal cost (dQ entries flagged), consumed by the combined bf16
+//     backward kernel.
+//
+// Two orders, chosen on the device per call:
+//   * cost-major: entries sorted by cost, longest first -- the makespan
+//     bound of longest-processing-time-first when the work per work-group
+//     is not far above the longest item;
+//   * sequence-major: sequence by sequence, longest sequence first, each
+//     sequence's entries longest first -- when the work per work-group is
+//     many times the longest item, so that balance is easy, the items that
+//     run at the same time stay on a few sequences, whose K/V (or Q/dO)
+//     rows they share through the caches.
 //
 // Built on the device from seq_offsets (no host round trip) by one
-// work-group: a histogram of tile counts, a descending exclusive scan of the
-// cost bins, then a scatter in which each entry takes the next slot of its
-// bin.  Order inside a bin is arbitrary; no result depends on it except the
-// summation order of the table gradients.
+// work-group: a histogram of tile counts, a rank per sequence (tile count
+// descending, ties in arbitrary order), then a scatter in which every entry's
+// slot follows from its sequence's rank.  No result depends on the order of
+// ties except the summation order of the table gradients.
 #pragma once
 
 #include "internal.h"
@@ -30,13 +42,18 @@ namespace hstu {
 
 constexpr int SCHED_MAX_BINS = 65536 / TILE + 2;   // max_len <= 65536
 
+// The sequence-major order needs this many times the longest item's cost of
+// work per work-group (in 64 x 64 tile pairs).
+constexpr int SCHED_SEQ_MAJOR_SLACK = 4;
+
 struct SchedSmem {
-  int32_t count_ge[SCHED_MAX_BINS];   // # sequences with ntiles == c
-  int32_t start[SCHED_MAX_BINS];      // first slot of cost bin c
-  int32_t fill_q[SCHED_MAX_BINS];
-  int32_t fill_k[SCHED_MAX_BINS];
-  int32_t ge[SCHED_MAX_BINS];         // # sequences with ntiles >= c
+  int32_t count[SCHED_MAX_BINS];      // # sequences with ntiles == n
+  int32_t rank0[SCHED_MAX_BINS];      // first rank of tile-count bin n (# with ntiles > n)
+  int32_t fill[SCHED_MAX_BINS];       // sequences ranked in bin n so far
+  int32_t cstart[SCHED_MAX_BINS];     // cost-major: first entry of cost bin c
+  int32_t sstart[SCHED_MAX_BINS];     // sequence-major: first entry of bin n's sequences
   int32_t total;
+  int32_t seq_major;
 };
 
 struct SchedArgs {
@@ -47,6 +64,8 @@ struct SchedArgs {
   SeqInfo *info;
   WorkEntry *list_q, *list_k, *list_b;
   int32_t nbins, cap;
+  int32_t H;
+  int32_t grid_hint;                  // nominal persistent work-groups
   float *zero_out;
   int32_t n_zero;
 };
@@ -56,9 +75,8 @@ template <int NT>
 __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm, int tid) {
   for (int x = tid; x < a.n_zero; x += NT) a.zero_out[x] = 0.0f;
   for (int c = tid; c < a.nbins; c += NT) {
-    sm.count_ge[c] = 0;
-    sm.fill_q[c] = 0;
-    sm.fill_k[c] = 0;
+    sm.count[c] = 0;
+    sm.fill[c] = 0;
   }
   if (tid == 0) sm.total = 0;
   __syncthreads();
@@ -76,22 +94,30 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     a.info[b].len = (int32_t)L;
     a.info[b].ntiles = nt;
     if (nt > 0) {
-      atomicAdd(&sm.count_ge[nt], 1);
+      atomicAdd(&sm.count[nt], 1);
       atomicAdd(&sm.total, nt);
     }
   }
   __syncthreads();
 
-  // Bin c (cost c) holds one entry per sequence with ntiles >= c; bins are
-  // laid out from the most expensive down.  Serial over at most 1026 bins.
+  // Ranks, bin starts of both orders, and the choice of order.  Serial over
+  // at most 1026 bins.
   if (tid == 0) {
-    int32_t run = 0, ge = 0;
-    for (int c = a.nbins - 1; c >= 1; --c) {
-      ge += sm.count_ge[c];        // sequences with ntiles >= c
-      sm.start[c] = run;
-      sm.ge[c] = ge;
-      run += ge;
+    int32_t ranks = 0, seq_run = 0, ge = 0, cost_run = 0, nt_max = 0;
+    int64_t work = 0;                              // causal tile pairs per head
+    for (int n = a.nbins - 1; n >= 1; --n) {
+      const int32_t c = sm.count[n];
+      if (c > 0 && nt_max == 0) nt_max = n;
+      sm.rank0[n] = ranks;
+      ranks += c;
+      sm.sstart[n] = seq_run;                      // sequences of n tiles, n entries each
+      seq_run += n * c;
+      ge += c;                                     // sequences with ntiles >= n
+      sm.cstart[n] = cost_run;                     // cost bin n: one entry per such sequence
+      cost_run += ge;
+      work += (int64_t)c * n * (n + 1) / 2;
     }
+    sm.seq_major = work * a.H >= (int64_t)SCHED_SEQ_MAJOR_SLACK * nt_max * a.grid_hint;
     // Valid offsets never exceed the list capacity; overlapping (invalid)
     // ones can, and then only the first `cap` slots are kept -- every slot
     // below the total is filled exactly once, so the kept prefix is dense.
@@ -103,24 +129,33 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
   }
   __syncthreads();
 
+  const bool seq_major = sm.seq_major != 0;
   for (int b = tid; b < a.B; b += NT) {
     const SeqInfo si = a.info[b];
     const int nt = si.ntiles;
+    if (nt == 0) continue;
+    const int r = sm.rank0[nt] + atomicAdd(&sm.fill[nt], 1);   // rank, by tile count
+    // sequence-major: this sequence's first entry
+    const int base = sm.sstart[nt] + (r - sm.rank0[nt]) * nt;
     for (int t = 0; t < nt; ++t) {
       const WorkEntry we{b, t, si.len, 0, si.start};
-      WorkEntry wq = we;
-      wq.tile |= BWD_DQ_FLAG;
       const int cq = t + 1;          // q-tile t visits k-tiles 0..t
       const int ck = nt - t;         // k-tile t is visited by q-tiles t..nt-1
-      const int sq = sm.start[cq] + atomicAdd(&sm.fill_q[cq], 1);
-      const int sk = sm.start[ck] + atomicAdd(&sm.fill_k[ck], 1);
+      // cost-major: cost bin c holds one entry per sequence with ntiles >= c,
+      // i.e. per rank below rank0[c] + count[c], in rank order
+      const int sq = seq_major ? base + (nt - 1 - t) : sm.cstart[cq] + r;
+      const int sk = seq_major ? base + t : sm.cstart[ck] + r;
       if (sq < a.cap) a.list_q[sq] = we;
       if (a.list_k && sk < a.cap) a.list_k[sk] = we;
       if (a.list_b) {
-        // combined backward list: bin c spans 2 ge[c] slots from 2 start[c],
-        // dK/dV entries first (the heavier item of equal cost), then dQ ones
-        const int bk = sk + sm.start[ck];
-        const int bq = sq + sm.start[cq] + sm.ge[cq];
+        // combined list: cost-major, bin c spans 2 ge(c) slots, its dK/dV
+        // entries then its dQ entries; sequence-major, per sequence the
+        // dK/dV then the dQ entry of each cost, from nt down to 1
+        WorkEntry wq = we;
+        wq.tile |= BWD_DQ_FLAG;
+        const int bk = seq_major ? 2 * base + 2 * t : 2 * sm.cstart[ck] + r;
+        const int bq = seq_major ? 2 * base + 2 * (nt - 1 - t) + 1
+                                 : 2 * sm.cstart[cq] + sm.rank0[cq] + sm.count[cq] + r;
         if (bk < 2 * a.cap) a.list_b[bk] = we;
         if (bq < 2 * a.cap) a.list_b[bq] = wq;
       }
@@ -143,6 +178,8 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.list_b = L.list_b ? (WorkEntry *)(base + L.list_b) : nullptr;
   a.nbins = (int)((p.N + TILE - 1) / TILE) + 2;
   a.cap = (int32_t)p.max_entries;
+  a.H = p.H;
+  a.grid_hint = 4 * L.num_cu;
   a.zero_out = L.dtime_part ? (float *)(base + L.dtime_part) : nullptr;
   a.n_zero = L.dtime_part ? DTIME_BINS * p.H * p.nb : 0;
   return a;

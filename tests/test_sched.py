@@ -1,6 +1,10 @@
 """seq_offsets tile scheduler: a host reference enumerator, its properties,
 and the device scheduler's work lists checked against it bit for bit (as
-multisets; order inside a cost bin is free)."""
+multisets), with their order.  The scheduler takes one of two orders:
+cost-major (every entry longest first) unless the causal work per nominal
+work-group is at least SLACK times the longest entry, then sequence-major
+(sequence by sequence, longest sequence first, order among equal lengths
+free, each sequence's tiles longest first)."""
 import itertools
 
 import numpy as np
@@ -8,6 +12,7 @@ import pytest
 import torch
 
 TILE = 64
+SLACK = 4          # work per work-group over the longest entry for sequence-major
 
 
 def reference_lists(lengths, N):
@@ -74,6 +79,50 @@ def test_lpt_within_graham_bound_bruteforce():
         assert lpt_makespan(costs, m) <= (4 / 3 - 1 / (3 * m)) * opt_makespan(costs, m) + 1e-9
 
 
+def sequence_major(lengths, N, H, grid):
+    """The scheduler's choice of order: causal tile pairs over all heads
+    against SLACK times the longest entry on every work-group."""
+    nt = (np.minimum(np.asarray(lengths), N) + TILE - 1) // TILE
+    if nt.size == 0 or nt.max() == 0:
+        return False
+    work = int((nt * (nt + 1) // 2).sum())
+    return work * H >= SLACK * int(nt.max()) * grid
+
+
+def check_order(got, nts, seq_major):
+    """got: [(cost, b, tile)] in pop order."""
+    if not seq_major:
+        costs = [c for c, _, _ in got]
+        assert costs == sorted(costs, reverse=True)
+        return
+    # contiguous per-sequence blocks, in non-increasing tile count
+    blocks = []
+    for c, b, t in got:
+        if not blocks or blocks[-1][0] != b:
+            assert all(b != bb for bb, _ in blocks), "sequence split across blocks"
+            blocks.append((b, []))
+        blocks[-1][1].append(c)
+    sizes = [int(nts[b]) for b, _ in blocks]
+    assert sizes == sorted(sizes, reverse=True)
+    # inside a block: costs nt, nt-1, ..., 1 (longest first)
+    for b, costs in blocks:
+        assert costs == list(range(int(nts[b]), 0, -1))
+
+
+def test_order_choice():
+    grid = 1024
+    assert not sequence_major([512] * 128, 512, 4, grid)      # 8 tiles, little work
+    assert sequence_major([8192] * 1024, 8192, 4, grid)       # deep batch
+    assert not sequence_major([], 64, 4, grid)
+    assert not sequence_major([0, 0], 64, 4, grid)
+    # the threshold itself: one sequence of nt tiles, nt (nt + 1) / 2 pairs
+    nt = 7
+    need = SLACK * nt * grid            # pairs x H
+    H = -(-need // (nt * (nt + 1) // 2))
+    assert not sequence_major([nt * TILE], nt * TILE, H - 1, grid)
+    assert sequence_major([nt * TILE], nt * TILE, H, grid)
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("seed,B,N", [(0, 7, 256), (1, 300, 512), (2, 1024, 8192), (3, 5, 64)])
 def test_device_lists_match_reference(seed, B, N):
@@ -91,5 +140,8 @@ def test_device_lists_match_reference(seed, B, N):
     got_q = [(t + 1, b, t) for b, t in lq.tolist()]
     got_k = [(int(nts[b]) - t, b, t) for b, t in lk.tolist()]
     assert sorted(got_q) == sorted(q) and sorted(got_k) == sorted(k)
-    assert all(got_q[i][0] >= got_q[i + 1][0] for i in range(len(got_q) - 1))
-    assert all(got_k[i][0] >= got_k[i + 1][0] for i in range(len(got_k) - 1))
+    grid = 4 * torch.cuda.get_device_properties(0).multi_processor_count
+    seq_major = sequence_major(lengths, N, 1, grid)
+    print(f"  order: {'sequence' if seq_major else 'cost'}-major", flush=True)
+    for got in (got_q, got_k):
+        check_order(got, nts, seq_major)
