@@ -343,7 +343,7 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
 // DMA-filled buffers and bias slices, and proves every wave is done with
 // tile kt-1, whose buffer then takes tile kt+1.  Items are pipelined: each
 // work-group's first two items are static (the list's head, longest first),
-// the pop for the item after next is issued when an item starts, and an
+// the pop for the item after next is issued in an item's first step, and an
 // item's last tile streams the next item's first key tile, query rows, bias
 // slice and timestamps, so no item starts with an exposed memory latency.
 template <int D, bool POS, bool TIME>
@@ -402,7 +402,6 @@ attn_fwd_kernel(KParams P) {
     const int64_t ts_i_item = ts_i, ts_start_item = ts_start;
 
     int nxt2 = 0;
-    if (tid == 0) nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
     const bool has_next = nxt < n_items;
     Item nit = it;
     if (has_next) nit = load_item(P, nxt);
@@ -427,11 +426,13 @@ attn_fwd_kernel(KParams P) {
         }
         if (far) sm.flag[fs] = 1;
       }
-      if (last && tid == 0) sm.next[item_no & 1] = nxt2;
       wait_vm();
       lds_barrier();
       const bool slow = TIME && sm.flag[fs] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 2) % 3] = 0;
+      // pop the item after next here, older than this step's loads, so that
+      // no wait for them also waits for the atomic
+      if (kt == 0 && tid == 0) nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
@@ -522,7 +523,9 @@ attn_fwd_kernel(KParams P) {
       }
     }
 
-    // sum the two key halves in the last tile's buffer, store O (bf16)
+    // the popped index goes out through the epilogue's barriers; sum the
+    // two key halves in the last tile's buffer, store O (bf16)
+    if (tid == 0) sm.next[item_no & 1] = nxt2;
     sum_store_tile<D>((float *)sm.tile[(phase - 1) & 1], oacc, wj == 0, wi, g, l32, tid,
                       P.out0 + ((it.start + (int64_t)qt * TILE) * P.H + h) * D,
                       row_stride, q_valid, 1.0f);
@@ -650,13 +653,37 @@ __device__ __forceinline__ float dsilu(float x) {
   return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f);
 }
 
+// The backward kernels' persistent loop: a work-group's first item is
+// static (its block index in the longest-first list) and every item pops the
+// one after it at its first tile step, next to that step's prefetch loads,
+// so the atomic's latency hides behind the step instead of separating
+// items.  The popped index travels through `nxt` (thread 0) and `slot`.
+__device__ __forceinline__ void pop_next(const KParams &P, int tid, int &nxt) {
+  if (tid == 0) nxt = atomicAdd(P.pop, 1) + (int)gridDim.x;
+}
+
+__device__ __forceinline__ int take_next(int *slot, int tid, int nxt) {
+  if (tid == 0) *slot = nxt;
+  lds_barrier();
+  return *slot;
+}
+
+// A work-list entry carries its sequence's start and length.
+__device__ __forceinline__ SeqInfo entry_seq(const WorkEntry &e) {
+  SeqInfo si;
+  si.start = e.start;
+  si.len = e.len;
+  si.ntiles = (e.len + TILE - 1) / TILE;
+  return si;
+}
+
 // --------------------------------------------------------------------- dQ
 // One q-stationary item: dQ_i = sum_{j<=i} dS_ij k_j for a 64-row query tile
 // of one head, recomputing S and dA = dO V^T tile by tile.
 template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, float *dyn,
                                         const int tid0, const WorkEntry e, const int h,
-                                        int &phase) {
+                                        int &phase, int &nxt) {
   constexpr int ST = D + RM_PAD;
     int tid = tid0;
     asm volatile("" : "+v"(tid));
@@ -666,7 +693,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wi = w & 1, wj = w >> 1;
 
-    const SeqInfo si = P.info[e.seq];
+    const SeqInfo si = entry_seq(e);
     const int qt = e.tile;
     const int q_valid = si.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
@@ -723,6 +750,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
+      if (kt == 0) pop_next(P, tid, nxt);
       if (kt < qt) {
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
@@ -856,7 +884,7 @@ template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx, float *dyn,
                                          double *tacc, const int tid0, const WorkEntry e,
                                          const int h, int &phase, float *&pend_p,
-                                         float &pend_v) {
+                                         float &pend_v, int &nxt) {
   constexpr int ST = D + RM_PAD;
   StreamSmem<D> &sm = smx.s;
     int tid = tid0;
@@ -867,7 +895,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wj = w & 1, wi = w >> 1;        // key half (stationary), query half
 
-    const SeqInfo si = P.info[e.seq];
+    const SeqInfo si = entry_seq(e);
     const int kt = e.tile;
     const int k_valid = si.len - kt * TILE;
     const int j_loc = 32 * wj + l32;
@@ -948,6 +976,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
+      if (qt == kt) pop_next(P, tid, nxt);
       if (qt + 1 < si.ntiles) {
         const int nv = si.len - (qt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
@@ -1151,21 +1180,19 @@ attn_bwd_kernel(KParams P) {
   const int tid0 = threadIdx.x;
   const int n_items = 2 * P.ctrl[CTRL_N_ENTRIES] * P.H;
   dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
+  lds_barrier();
   int phase = 0;
   float *pend_p = nullptr;
   float pend_v = 0.0f;
-  for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
+  int nxt = 0;
+  for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt)) {
     WorkEntry e = P.list[item / P.H];
     const int h = item % P.H;
     if (e.tile & BWD_DQ_FLAG) {
       e.tile &= ~BWD_DQ_FLAG;
-      dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase);
+      dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase, nxt);
     } else {
-      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v);
+      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt);
     }
   }
   dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
@@ -1181,14 +1208,11 @@ attn_bwd_dq_kernel(KParams P) {
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
   if (TIME) stage_all_heads(P, dyn_q, tid0, 1.0f);
   if (tid0 < 2) sm.flag[tid0] = 0;
+  lds_barrier();
   int phase = 0;
-  for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
-    dq_item<D, POS, TIME>(P, sm, dyn_q, tid0, P.list[item / P.H], item % P.H, phase);
-  }
+  int nxt = 0;
+  for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt))
+    dq_item<D, POS, TIME>(P, sm, dyn_q, tid0, P.list[item / P.H], item % P.H, phase, nxt);
 }
 
 // Backward, dK/dV and the table gradients: persistent work-groups pop k-tile
@@ -1204,17 +1228,14 @@ attn_bwd_dkv_kernel(KParams P) {
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
   dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
+  lds_barrier();
   int phase = 0;
   float *pend_p = nullptr;
   float pend_v = 0.0f;
-  for (;;) {
-    if (tid0 == 0) sm.item = atomicAdd(P.pop, 1);
-    lds_barrier();
-    const int item = sm.item;
-    if (item >= n_items) break;
+  int nxt = 0;
+  for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt))
     dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, P.list[item / P.H], item % P.H, phase,
-                           pend_p, pend_v);
-  }
+                           pend_p, pend_v, nxt);
   dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
 }
 
