@@ -699,17 +699,27 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     const int i_loc = 32 * wi + l32;
     const int64_t qoff = ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
 
+    // every load of the item's start is issued before any of them is used,
+    // so the start costs one memory latency; timestamps of rows past the
+    // sequence repeat its last row (those rows are always masked)
     bf16x8 qreg[D / 16], doreg[D / 16];
     load_stationary<D>(P.q + qoff, i_loc, q_valid, row_stride, g, qreg);
     load_stationary<D>(P.dO + qoff, i_loc, q_valid, row_stride, g, doreg);
+    TileRegs<D> kr, vr;
+    kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
+    vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
+    int64_t ts_start = 0, ts_i = 0, ts_k = 0;
+    if (TIME) {
+      ts_start = P.ts[si.start];
+      ts_i = P.ts[si.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
+      if (tid < TILE) ts_k = P.ts[si.start + (tid < si.len ? tid : si.len - 1)];
+    }
+    float pos_v = POS ? pos_fetch(P, h, qt, 0, tid, 1.0f) : 0.0f;
 
-    int64_t ts_start = 0, ts_i = 0;
     int32_t ts_i32 = 0;
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
-      ts_start = P.ts[si.start];
-      ts_i = i_loc < q_valid ? P.ts[si.start + (int64_t)qt * TILE + i_loc] : ts_start;
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
@@ -721,16 +731,6 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[db][r] = 0.0f;
-
-    TileRegs<D> kr, vr;
-    int64_t ts_k = 0;
-    float pos_v = 0.0f;
-    {
-      kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
-      vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
-      if (TIME && tid < TILE) ts_k = tid < si.len ? P.ts[si.start + tid] : ts_start;
-      if (POS) pos_v = pos_fetch(P, h, qt, 0, tid, 1.0f);
-    }
 
     for (int kt = 0; kt <= qt; ++kt, ++phase) {
       lds_barrier();
@@ -756,7 +756,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
-        if (TIME && tid < TILE) ts_k = tid < k_valid ? P.ts[r0 + tid] : ts_start;
+        if (TIME && tid < TILE) ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
       }
 
@@ -915,13 +915,25 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
     }
 
-    int64_t ts_start = 0, ts_j = 0;
+    // every load of the item's start is issued before any of them is used
+    // (one memory latency); timestamps of rows past the sequence repeat its
+    // last row (those rows are always masked)
+    TileRegs<D> qr, dr;
+    const int64_t r0k = si.start + (int64_t)kt * TILE;
+    qr.load(P.q + (r0k * P.H + h) * D, k_valid, row_stride, tid);
+    dr.load(P.dO + (r0k * P.H + h) * D, k_valid, row_stride, tid);
+    int64_t ts_start = 0, ts_j = 0, ts_q = 0;
+    if (TIME) {
+      ts_start = P.ts[si.start];
+      ts_j = P.ts[r0k + (j_loc < k_valid ? j_loc : k_valid - 1)];
+      if (tid < TILE) ts_q = P.ts[r0k + (tid < k_valid ? tid : k_valid - 1)];
+    }
+    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, 1.0f) : 0.0f;
+
     int32_t ts_j32 = 0;
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
-      ts_start = P.ts[si.start];
-      ts_j = j_loc < k_valid ? P.ts[si.start + (int64_t)kt * TILE + j_loc] : ts_start;
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
@@ -936,16 +948,6 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) { dk[db][r] = 0.0f; dv[db][r] = 0.0f; }
-
-    TileRegs<D> qr, dr;
-    int64_t ts_q = 0;
-    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, 1.0f) : 0.0f;
-    {
-      const int64_t r0 = si.start + (int64_t)kt * TILE;
-      qr.load(P.q + (r0 * P.H + h) * D, k_valid, row_stride, tid);
-      dr.load(P.dO + (r0 * P.H + h) * D, k_valid, row_stride, tid);
-      if (TIME && tid < TILE) ts_q = tid < k_valid ? P.ts[r0 + tid] : ts_start;
-    }
     if constexpr (KV_LDS) wait_vm();    // the first step's barriers publish the tiles
 
     for (int qt = kt; qt < si.ntiles; ++qt, ++phase) {
@@ -982,7 +984,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
         qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
         dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
-        if (TIME && tid < TILE) ts_q = tid < nv ? P.ts[r0 + tid] : ts_start;
+        if (TIME && tid < TILE) ts_q = P.ts[r0 + (tid < nv ? tid : nv - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, 1.0f);
       }
 
