@@ -6,9 +6,13 @@
 //   backward  du = n * dy;  g = dy * u;
 //             dO = rstd * (g - mean(g) - n * mean(g * n)),  n = (o - mean) * rstd
 //
-// One wave64 per token: each lane owns 8 consecutive features per 512-wide
-// chunk (one 16-byte bf16 load), statistics by wave shuffles.  These kernels
-// are HBM-bound (each feature is read and written once or twice).
+// When a token's F = H*d features are 8 x (a power of two <= 64) -- F <= 512,
+// every configuration of the benchmarks -- a wave holds 64/(F/8) whole tokens,
+// each lane 8 consecutive features of one token loaded once (16 bytes per
+// bf16 tensor, every load of the token issued before the first use), and the
+// statistics are shuffle sums over the token's lane group.  Otherwise one
+// wave64 walks a token in 512-wide chunks.  These kernels are HBM-bound
+// (each feature is read and written once or twice).
 #include <algorithm>
 
 #include "internal.h"
@@ -65,6 +69,87 @@ struct Vec8<float> {
   }
 };
 
+// Sum over the aligned group of L lanes (L a power of two) holding one token.
+template <int L>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+  for (int m = L / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+
+// Fast path: F = 8 L, L = 64 / TPW lanes per token, TPW tokens per wave.
+template <typename T, int L>
+__global__ void __launch_bounds__(LN_THREADS)
+ln_fwd_group_kernel(const T *__restrict__ o, const T *__restrict__ u,
+                    T *__restrict__ y, float *__restrict__ mean_out,
+                    float *__restrict__ rstd_out, int64_t T_tokens) {
+  constexpr int F = 8 * L, TPW = 64 / L;
+  const int lane = threadIdx.x & 63, sub = lane % L;
+  const int64_t r = ((int64_t)blockIdx.x * LN_WAVES + (threadIdx.x >> 6)) * TPW + lane / L;
+  if (r >= T_tokens) return;
+  const int64_t at = r * F + 8 * sub;
+  float z[8], uu[8];
+  Vec8<T>::load(o + at, z);
+  Vec8<T>::load(u + at, uu);
+  float sum = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sum += z[e];
+  const float mu = group_sum<L>(sum) / (float)F;
+  float sq = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sq += (z[e] - mu) * (z[e] - mu);
+  const float rstd = rsqrtf(group_sum<L>(sq) / (float)F + HSTU_LN_EPS);
+  float out[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) out[e] = (z[e] - mu) * rstd * uu[e];
+  Vec8<T>::store(y + at, out);
+  if (sub == 0) {
+    mean_out[r] = mu;
+    rstd_out[r] = rstd;
+  }
+}
+
+template <typename T, int L>
+__device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *__restrict__ u,
+                                             const T *__restrict__ o,
+                                             const float *__restrict__ mean,
+                                             const float *__restrict__ rstd,
+                                             T *__restrict__ du, T *__restrict__ dO,
+                                             float *__restrict__ dpos_part, int H,
+                                             int64_t T_tokens, int block) {
+  constexpr int F = 8 * L, TPW = 64 / L;
+  const int lane = threadIdx.x & 63, sub = lane % L;
+  const int64_t r = ((int64_t)block * LN_WAVES + (threadIdx.x >> 6)) * TPW + lane / L;
+  if (r >= T_tokens) return;
+  const int64_t at = r * F + 8 * sub;
+  float z[8], g[8], uu[8];
+  Vec8<T>::load(o + at, z);
+  Vec8<T>::load(dy + at, g);
+  Vec8<T>::load(u + at, uu);
+  const float mu = mean[r], rs = rstd[r];
+  float sg = 0.0f, sgn = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float n = (z[e] - mu) * rs;
+    const float gg = g[e] * uu[e];
+    sg += gg;
+    sgn += gg * n;
+  }
+  const float mg = group_sum<L>(sg) / (float)F;
+  const float mgn = group_sum<L>(sgn) / (float)F;
+  float o_du[8], o_do[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float n = (z[e] - mu) * rs;
+    o_du[e] = n * g[e];
+    o_do[e] = rs * (g[e] * uu[e] - mg - n * mgn);
+  }
+  Vec8<T>::store(du + at, o_du);
+  Vec8<T>::store(dO + at, o_do);
+  // the attention backward accumulates this token's d_pos partials
+  if (dpos_part && sub < H) dpos_part[r * H + sub] = 0.0f;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(LN_THREADS)
 ln_fwd_kernel(const T *__restrict__ o, const T *__restrict__ u,
@@ -118,6 +203,19 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
     __shared__ SchedSmem ssm;
     build_schedule<LN_THREADS>(sa, ssm, threadIdx.x);
     return;
+  }
+  // F = 8 x (power of two <= 64): whole tokens per lane group
+  switch (F) {
+#define HSTU_LN_GROUP(LL)                                                               \
+  case 8 * LL:                                                                          \
+    ln_bwd_group<T, LL>(dy, u, o, mean, rstd, du, dO, dpos_part, H, T_tokens,            \
+                        (int)blockIdx.x - sched);                                       \
+    return;
+    HSTU_LN_GROUP(1) HSTU_LN_GROUP(2) HSTU_LN_GROUP(4) HSTU_LN_GROUP(8)
+    HSTU_LN_GROUP(16) HSTU_LN_GROUP(32) HSTU_LN_GROUP(64)
+#undef HSTU_LN_GROUP
+    default:
+      break;
   }
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)(blockIdx.x - sched) * LN_WAVES + (threadIdx.x >> 6);
@@ -229,17 +327,47 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
 
 }  // namespace
 
+// Lanes per token of the fast path (F = 8 L, L a power of two <= 64), else 0.
+static int ln_group_lanes(int F) {
+  if (F % 8 != 0 || F > 512) return 0;
+  const int L = F / 8;
+  return (L & (L - 1)) == 0 ? L : 0;
+}
+
+// Work-groups covering T tokens, LN_WAVES waves of `tpw` tokens each.
+static unsigned ln_blocks(int64_t T, int tpw) {
+  const int64_t per = (int64_t)LN_WAVES * tpw;
+  return (unsigned)((T + per - 1) / per);
+}
+
+template <typename T>
+hipError_t launch_ln_fwd_t(const Problem &p, const T *o, const T *u, T *y, float *mean,
+                           float *rstd, hipStream_t s) {
+  const int F = p.H * p.d;
+  const int L = ln_group_lanes(F);
+  switch (L) {
+#define HSTU_LN_GROUP(LL)                                                               \
+  case LL:                                                                              \
+    hipLaunchKernelGGL((ln_fwd_group_kernel<T, LL>), dim3(ln_blocks(p.T, 64 / LL)),      \
+                       dim3(LN_THREADS), 0, s, o, u, y, mean, rstd, p.T);               \
+    return hipGetLastError();
+    HSTU_LN_GROUP(1) HSTU_LN_GROUP(2) HSTU_LN_GROUP(4) HSTU_LN_GROUP(8)
+    HSTU_LN_GROUP(16) HSTU_LN_GROUP(32) HSTU_LN_GROUP(64)
+#undef HSTU_LN_GROUP
+    default:
+      break;
+  }
+  hipLaunchKernelGGL(ln_fwd_kernel<T>, dim3(ln_blocks(p.T, 1)), dim3(LN_THREADS), 0, s, o, u,
+                     y, mean, rstd, p.T, F);
+  return hipGetLastError();
+}
+
 hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
                          void *y, float *mean, float *rstd, hipStream_t s) {
-  const int F = p.H * p.d;
-  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES));
   if (p.dtype == HSTU_BF16)
-    hipLaunchKernelGGL(ln_fwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
-                       (const u16 *)o, (const u16 *)u, (u16 *)y, mean, rstd, p.T, F);
-  else
-    hipLaunchKernelGGL(ln_fwd_kernel<float>, grid, dim3(LN_THREADS), 0, s,
-                       (const float *)o, (const float *)u, (float *)y, mean, rstd, p.T, F);
-  return hipGetLastError();
+    return launch_ln_fwd_t<u16>(p, (const u16 *)o, (const u16 *)u, (u16 *)y, mean, rstd, s);
+  return launch_ln_fwd_t<float>(p, (const float *)o, (const float *)u, (float *)y, mean, rstd,
+                                s);
 }
 
 hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
@@ -249,7 +377,8 @@ hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
                                hipStream_t s) {
   const int F = p.H * p.d;
   const SchedArgs sa = sched_args(seq_offsets, p, ws, L);
-  const dim3 grid((unsigned)((p.T + LN_WAVES - 1) / LN_WAVES) + 1);
+  const int GL = ln_group_lanes(F);
+  const dim3 grid(ln_blocks(p.T, GL ? 64 / GL : 1) + 1);
   if (p.dtype == HSTU_BF16)
     hipLaunchKernelGGL(ln_bwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
                        (const u16 *)dy, (const u16 *)u, (const u16 *)o, mean, rstd,
