@@ -335,7 +335,7 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
     ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, L2E);
+  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, 1.0f);
 }
 
 // ---------------------------------------------------------------- forward
@@ -440,7 +440,7 @@ attn_fwd_kernel(KParams P) {
         dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, L2E);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
       } else if (has_next) {   // ... or the next item's first one
         fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
                                      tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
@@ -448,10 +448,22 @@ attn_fwd_kernel(KParams P) {
       const u16 *kt_lds = sm.tile[pb][0];
       const u16 *vt_lds = sm.tile[pb][1];
 
-      // S^T quadrant [32 keys x 32 queries] = K_wj Q_wi^T
+      // S^T quadrant [32 keys x 32 queries] = K_wj Q_wi^T, with the position
+      // bias as the accumulator's initial value; this lane's keys sit at
+      // 32 wj + 4 g + 8 q4 + c
+      const int kb = 32 * wj + 4 * g;
       f32x16 s;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+      if (POS) {
+        const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 pbv = *(const float4 *)(pl + 8 * q4);
+          s[4 * q4 + 0] = pbv.x; s[4 * q4 + 1] = pbv.y;
+          s[4 * q4 + 2] = pbv.z; s[4 * q4 + 3] = pbv.w;
+        }
+      }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks)
         s = mfma32(sread_rm<D>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
@@ -459,29 +471,14 @@ attn_fwd_kernel(KParams P) {
         load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
                            i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
 
-      // x' = s log2e + bias', A = silu(x)/N, then O_wi += A V, one 16-key
-      // half at a time (half the temporaries live at once); this lane's
-      // keys sit at 32 wj + 4 g + 8 q4 + c
-      const int kb = 32 * wj + 4 * g;
+      // x' = (s + pos) log2e + time bias', A = silu(x)/N, then O_wi += A V,
+      // one 16-key half at a time (half the temporaries live at once)
       const float nl = (float)P.N * L2E;
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         float x[8];
-        if (POS) {
-          const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
 #pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const int q4 = 2 * hh + q;
-            const float4 pbv = *(const float4 *)(pl + 8 * q4);
-            x[4 * q + 0] = __builtin_fmaf(s[4 * q4 + 0], L2E, pbv.x);
-            x[4 * q + 1] = __builtin_fmaf(s[4 * q4 + 1], L2E, pbv.y);
-            x[4 * q + 2] = __builtin_fmaf(s[4 * q4 + 2], L2E, pbv.z);
-            x[4 * q + 3] = __builtin_fmaf(s[4 * q4 + 3], L2E, pbv.w);
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e] * L2E;
-        }
+        for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e] * L2E;
         if (TIME) {
           if (!slow) {
 #pragma unroll
