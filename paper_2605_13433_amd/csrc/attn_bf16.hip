@@ -717,6 +717,9 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
+      // the work-group's tables, staged at its first item after that item's
+      // loads (both latencies overlap)
+      if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
@@ -931,6 +934,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
+      if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);   // as in dq_item
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
@@ -1133,15 +1137,14 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
 }
 
 // Work-group start of the kernels that run dK/dV items: zeroed d_time
-// histogram and index accumulators, staged time tables, cleared flags and
-// d_pos windows.
+// histogram and index accumulators, cleared flags and d_pos windows (the
+// time tables are staged by the first item).
 template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dkv_kernel_init(const KParams &P, DkvSmem<D, POS> &smx,
                                                 double *tacc, float *dyn, int tid0) {
   if (TIME) {
     for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
     for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0;
-    stage_all_heads(P, dyn, tid0, 1.0f);
   }
   if (tid0 < 2) smx.s.flag[tid0] = 0;
   if constexpr (POS)
@@ -1205,7 +1208,6 @@ attn_bwd_dq_kernel(KParams P) {
   extern __shared__ float dyn_q[];            // time tables
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  if (TIME) stage_all_heads(P, dyn_q, tid0, 1.0f);
   if (tid0 < 2) sm.flag[tid0] = 0;
   lds_barrier();
   int phase = 0;
