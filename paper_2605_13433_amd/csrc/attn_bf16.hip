@@ -342,8 +342,9 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
 // One work-group barrier per key tile: the barrier of tile kt publishes its
 // DMA-filled buffers and bias slices, and proves every wave is done with
 // tile kt-1, whose buffer then takes tile kt+1.  Items are pipelined: each
-// work-group's first two items are static (the list's head, longest first),
-// the pop for the item after next is issued in an item's first step, and an
+// work-group's first two items are static (the list's head, longest first,
+// the second ones paired in reverse), the pop for the item after next is
+// issued one step before an item's last, and an
 // item's last tile streams the next item's first key tile, query rows, bias
 // slice and timestamps, so no item starts with an exposed memory latency.
 template <int D, bool POS, bool TIME>
@@ -353,7 +354,9 @@ attn_fwd_kernel(KParams P) {
   extern __shared__ float dyn[];              // time tables (see item_time_slot)
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
   int cur = blockIdx.x;
-  int nxt = gridDim.x + blockIdx.x;
+  // second static item: the list's next G items paired in reverse, so the
+  // work-group with the longest first item gets the shortest second one
+  int nxt = 2 * gridDim.x - 1 - blockIdx.x;
   if (cur >= n_items) return;
   const int tid0 = threadIdx.x;
   if (tid0 < 3) sm.flag[tid0] = 0;
@@ -430,9 +433,11 @@ attn_fwd_kernel(KParams P) {
       lds_barrier();
       const bool slow = TIME && sm.flag[fs] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 2) % 3] = 0;
-      // pop the item after next here, older than this step's loads, so that
-      // no wait for them also waits for the atomic
-      if (kt == 0 && tid == 0) nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
+      // pop the item after next one step before the last (as late as the
+      // atomic's latency allows), older than this step's loads, so that no
+      // wait for them also waits for the atomic
+      if (kt == (qt > 0 ? qt - 1 : 0) && tid == 0)
+        nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
@@ -652,9 +657,10 @@ __device__ __forceinline__ float dsilu(float x) {
 
 // The backward kernels' persistent loop: a work-group's first item is
 // static (its block index in the longest-first list) and every item pops the
-// one after it at its first tile step, next to that step's prefetch loads,
-// so the atomic's latency hides behind the step instead of separating
-// items.  The popped index travels through `nxt` (thread 0) and `slot`.
+// one after it at its last tile step, so the atomic's latency hides behind
+// that step instead of separating items, while a work-group still takes its
+// next item only when it is nearly free (greedy longest-first assignment).
+// The popped index travels through `nxt` (thread 0) and `slot`.
 __device__ __forceinline__ void pop_next(const KParams &P, int tid, int &nxt) {
   if (tid == 0) nxt = atomicAdd(P.pop, 1) + (int)gridDim.x;
 }
@@ -750,7 +756,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
-      if (kt == 0) pop_next(P, tid, nxt);
+      if (kt == qt) pop_next(P, tid, nxt);
       if (kt < qt) {
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
@@ -979,7 +985,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
-      if (qt == kt) pop_next(P, tid, nxt);
+      if (qt + 1 == si.ntiles) pop_next(P, tid, nxt);
       if (qt + 1 < si.ntiles) {
         const int nv = si.len - (qt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
