@@ -2,7 +2,7 @@
 // QKV with the relative position and relative time biases fused into the
 // attention kernel, no padding and no dense<->jagged conversion).
 //
-// Two persistent kernels pop (sequence, 64-row tile, head) items from the
+// Persistent kernels pop (sequence, 64-row tile, head) items from the
 // scheduler's longest-first lists:
 //
 //   attn_fwd   q-stationary: O_i = sum_{j<=i} silu(s_ij)/N v_j
@@ -25,15 +25,17 @@
 // Work-group = 4 wave64s on a 64x64 tile pair; each wave owns a 32x32
 // quadrant (half of the stationary rows x half of the streamed rows) and all
 // contractions use the 32x32x16 bf16 MFMA.  The stationary operand lives in
-// registers.  The streamed tile is staged in LDS once, row-major: the
-// score-side products read it along d with 16-byte loads, the accumulating
-// products (contracted over tile rows) read it through the gfx950 LDS
-// transpose load, which hands each lane one column of 4 consecutive rows.
-// Score accumulators come out with one fixed stationary row per lane, which
-// is exactly the operand layout of the accumulating product, so scores
-// never leave registers.  The two halves of the streamed side are summed
-// through LDS once per item.  The next streamed tile (with its bias slice and
-// timestamps) is fetched into registers while the current one computes.
+// registers (the dK/dV items' K and V at d=64: in LDS).  The streamed tile is
+// staged in LDS once: the score-side products read it along d with 16-byte
+// loads, the accumulating products (contracted over tile rows) read it
+// through the gfx950 LDS transpose load, which hands each lane one column of
+// 4 consecutive rows.  Score accumulators come out with one fixed stationary
+// row per lane, which is exactly the operand layout of the accumulating
+// product, so scores never leave registers.  The two halves of the streamed
+// side are summed through LDS once per item.  The next streamed tile (with
+// its bias slice and timestamps) is fetched while the current one computes:
+// straight into LDS by global-to-LDS loads in the forward, through registers
+// in the backward.
 //
 // Relative-time bias fast path: while every timestamp of the tile pair lies
 // within 2^23 of the sequence's first one, |ts_i - ts_j| < 2^24 converts to
