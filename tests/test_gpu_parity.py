@@ -71,6 +71,46 @@ def test_small_f32(d):
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
+def far_timestamps(lengths, seed):
+    """Timestamps that drive the exact time-bucket path: per sequence (in
+    order) mostly small gaps with a few of 2^22..2^31 s (tiles go from near
+    to far of the sequence's first timestamp part-way), every gap about 2^26 s
+    (deltas beyond 32 bits), small gaps only (fast path), and small gaps in
+    shuffled order (negative deltas, non-monotone index runs)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for b, L in enumerate(lengths):
+        kind = b % 4
+        g = 1 + np.floor(rng.exponential(600.0, size=L)).astype(np.int64)
+        if kind == 0:
+            big = rng.random(L) < 0.05
+            g[big] = rng.integers(1 << 22, 1 << 31, size=int(big.sum()))
+        elif kind == 1:
+            g = rng.integers(1 << 25, 1 << 27, size=L)
+        ts = np.cumsum(g)
+        ts -= ts[0] if L else 0
+        if kind == 3:
+            rng.shuffle(ts)
+        out.append(ts)
+    return torch.from_numpy(np.concatenate(out).astype(np.int64))
+
+
+@pytest.mark.parametrize("d,dtype", [(64, torch.bfloat16), (128, torch.bfloat16),
+                                     (64, torch.float32)])
+def test_far_timestamps(d, dtype):
+    lengths = [200, 130, 65, 150, 64, 1, 250, 190]
+    say(f"far timestamps d={d} {dtype}: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=2, d=d, N=256, dtype=dtype, seed=300 + d)
+    w.timestamps = far_timestamps(lengths, seed=301)
+    ts = w.timestamps.numpy()
+    off = w.seq_offsets.numpy()
+    far = sum(int((np.abs(ts[off[b]:off[b + 1]] - ts[off[b]]) >= 1 << 23).any())
+              for b in range(len(lengths)) if off[b + 1] > off[b])
+    assert far >= 3
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
 def test_workload1_fp32_forward():
     w = inputs.workload(1)
     say(f"workload 1 {w.name}: T={w.T} pairs/head={w.pairs}")
