@@ -111,6 +111,17 @@ def test_far_timestamps(d, dtype):
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
+def test_long_sequence():
+    """One sequence longer than any workload's (141 tiles, ragged last tile)
+    beside short ones: tile indices, bias-table spans and scheduler bins past
+    the workloads' range."""
+    lengths = [9000, 300, 1, 64]
+    say(f"long sequence: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=1, d=64, N=9000, seed=400)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
 def test_workload1_fp32_forward():
     w = inputs.workload(1)
     say(f"workload 1 {w.name}: T={w.T} pairs/head={w.pairs}")
