@@ -614,7 +614,8 @@ struct StreamSmem {
     float red[2][32 * D];                // cross-wave sums at the end of an item
   };
   alignas(16) float pos[4 * POS_COPY];
-  alignas(16) int32_t ts32[TILE];        // streamed-tile timestamps - ts_start
+  alignas(16) float ts32[TILE];          // streamed-tile timestamps - ts_start (exact
+                                         // floats on the fast path, |value| < 2^23)
   int64_t ts64[TILE];                    // raw streamed-tile timestamps
   int flag[2];                           // "some timestamp is far" (parity-buffered)
   int item;
@@ -642,11 +643,6 @@ struct TimeRun {
   }
 };
 
-
-// Integer time difference -> float-exponent index (|delta| < 2^24).
-__device__ __forceinline__ int time_index(int32_t delta) {
-  return (int)__builtin_amdgcn_ubfe(__float_as_uint((float)delta), 21u, 10u);
-}
 
 // silu'(x) = sigma(x) (1 + x (1 - sigma(x))).  The backward kernels work
 // with N dS and N A (the 1/N of both is applied once, to the accumulated
@@ -721,7 +717,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     }
     float pos_v = POS ? pos_fetch(P, h, qt, 0, tid, 1.0f) : 0.0f;
 
-    int32_t ts_i32 = 0;
+    float ts_i32 = 0.0f;
     bool q_far = false;
     float *ktab = dyn;
     if (TIME) {
@@ -729,7 +725,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       // loads (both latencies overlap)
       if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);
       const int64_t rel = ts_i - ts_start;
-      ts_i32 = (int32_t)rel;
+      ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
       ktab = item_time_slot(P, dyn, h, tid, 1.0f);
     }
@@ -749,7 +745,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         bool far = q_far;
         if (tid < TILE) {
           const int64_t rel = ts_k - ts_start;
-          sm.ts32[tid] = (int32_t)rel;
+          sm.ts32[tid] = (float)(int32_t)rel;
           sm.ts64[tid] = ts_k;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -800,7 +796,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
           if (!slow) {
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
-              const int4 t4 = *(const int4 *)(sm.ts32 + kb + 8 * (2 * hh + q));
+              const float4 t4 = *(const float4 *)(sm.ts32 + kb + 8 * (2 * hh + q));
               x[4 * q + 0] += ktab[time_index(ts_i32 - t4.x)];
               x[4 * q + 1] += ktab[time_index(ts_i32 - t4.y)];
               x[4 * q + 2] += ktab[time_index(ts_i32 - t4.z)];
@@ -938,13 +934,13 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     }
     float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, 1.0f) : 0.0f;
 
-    int32_t ts_j32 = 0;
+    float ts_j32 = 0.0f;
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
       if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);   // as in dq_item
       const int64_t rel = ts_j - ts_start;
-      ts_j32 = (int32_t)rel;
+      ts_j32 = (float)(int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
       ktab = item_time_slot(P, dyn, h, tid, 1.0f);
     }
@@ -978,7 +974,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         bool far = k_far;
         if (tid < TILE) {
           const int64_t rel = ts_q - ts_start;
-          sm.ts32[tid] = (int32_t)rel;
+          sm.ts32[tid] = (float)(int32_t)rel;
           sm.ts64[tid] = ts_q;
           far |= rel >= NEAR || rel <= -NEAR;
         }
@@ -1046,7 +1042,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
           if (!slow) {
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
-              const int4 t4 = *(const int4 *)(sm.ts32 + ib + 8 * (2 * hh + q));
+              const float4 t4 = *(const float4 *)(sm.ts32 + ib + 8 * (2 * hh + q));
               tk[4 * q + 0] = time_index(t4.x - ts_j32);
               tk[4 * q + 1] = time_index(t4.y - ts_j32);
               tk[4 * q + 2] = time_index(t4.z - ts_j32);
