@@ -32,10 +32,10 @@
  *
  * Pointers.  Every tensor pointer is a DEVICE pointer on the current HIP
  * device; the caller owns all memory.  The attention calls never allocate
- * device memory (for the layer calls see their section); no call
- * synchronises: each call enqueues its kernels on `stream`
- * (a hipStream_t; NULL = the default stream) and returns.  Buffers must stay
- * alive until that work completes.
+ * device memory and never synchronise (for the layer calls see their
+ * section): each call enqueues its kernels on `stream` (a hipStream_t; NULL
+ * = the default stream) and returns.  Buffers must stay alive until that
+ * work completes.
  *
  * seq_offsets contract (int64, device): off[0] = 0, non-decreasing,
  * 0 <= off[b+1] - off[b] <= max_len, off[B] = total_tokens.  It is read on
@@ -158,10 +158,14 @@ size_t hstu_jagged_attn_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
  * 1 <= d_model <= 65536 and d_model % 8 == 0.  Weights are row-major:
  * w1 [d_model][4*H*d], w2 [H*d][d_model]; x, out, dx [T][d_model].
  *
- * Allocation: the first layer call on a device creates that device's
- * hipBLASLt handle (hipBLASLt may allocate its own state then) and each new
- * GEMM shape runs one algorithm query; both are cached for the process.
- * GEMM scratch comes from the caller's workspace.  Thread-safe.
+ * Allocation and synchronisation: the first layer call on a device creates
+ * that device's hipBLASLt handle (hipBLASLt may allocate its own state then)
+ * and each new GEMM shape runs one algorithm query; the first call of a
+ * shape on a stream that is not being captured into a graph also times the
+ * query's candidate algorithms on the call's own operands and keeps the
+ * fastest -- that call waits for its stream once.  Everything is cached for
+ * the process; later calls never synchronise.  GEMM scratch comes from the
+ * caller's workspace.  Thread-safe.
  * ------------------------------------------------------------------------- */
 typedef struct {
     hstu_dtype dtype;            /* HSTU_BF16                                */

@@ -44,6 +44,10 @@ struct GemmPlan {
   hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr;
   hipblasLtMatmulAlgo_t algo;
   size_t ws = 0;
+  // The heuristic's candidates; the first call of the shape outside graph
+  // capture times them and keeps the fastest.
+  std::vector<hipblasLtMatmulAlgo_t> cands;
+  bool tuned = false;
 };
 
 void destroy(GemmPlan &g) {
@@ -136,8 +140,56 @@ int get_plan(int dev, const GemmShape &g, GemmPlan **out) {
   }
   p.algo = res[pick].algo;
   p.ws = res[pick].workspaceSize;
+  for (int i = pick; i < n; ++i)
+    if (res[i].state == HIPBLAS_STATUS_SUCCESS && res[i].workspaceSize <= GEMM_WS_BYTES)
+      p.cands.push_back(res[i].algo);
   *out = &db.plans.emplace(g, p).first->second;
   return HSTU_OK;
+}
+
+// Times every candidate algorithm of plan `p` on the call's own operands
+// (two runs each, the second timed; C is rewritten by the call that
+// follows) and keeps the fastest.  Skipped while `s` is being captured into
+// a graph (no synchronisation is allowed there): the heuristic's first
+// choice stays until an uncaptured call.  Returns false on a HIP error.
+bool tune_plan(int dev, GemmPlan *p, const void *A, const void *B, void *C, void *ws,
+               hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return false;
+  if (cs != hipStreamCaptureStatusNone || p->cands.size() < 2) {
+    p->tuned = cs == hipStreamCaptureStatusNone;
+    return true;
+  }
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) hipEventDestroy(e0);
+    return false;
+  }
+  const float alpha = 1.0f, beta = 0.0f;
+  float best_ms = 0.0f;
+  int best = -1;
+  for (size_t i = 0; i < p->cands.size(); ++i) {
+    bool ok = true;
+    for (int rep = 0; rep < 2 && ok; ++rep) {
+      if (rep == 1) ok = hipEventRecord(e0, s) == hipSuccess;
+      ok = ok && hipblasLtMatmul(g_blas[dev].handle, p->op, &alpha, B, p->la, A, p->lb,
+                                 &beta, C, p->lc, C, p->lc, &p->cands[i], ws,
+                                 GEMM_WS_BYTES, s) == HIPBLAS_STATUS_SUCCESS;
+      if (rep == 1) ok = ok && hipEventRecord(e1, s) == hipSuccess;
+    }
+    float ms = 0.0f;
+    if (ok && hipEventSynchronize(e1) == hipSuccess &&
+        hipEventElapsedTime(&ms, e0, e1) == hipSuccess && (best < 0 || ms < best_ms)) {
+      best = (int)i;
+      best_ms = ms;
+    }
+  }
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  if (best >= 0) p->algo = p->cands[best];
+  p->tuned = true;
+  (void)hipGetLastError();   // a candidate that failed to launch left no state
+  return true;
 }
 
 // Row-major C = op(A) . op(B) on `s`; `ws` holds GEMM_WS_BYTES.
@@ -147,6 +199,8 @@ int gemm(int dev, const GemmShape &g, const void *A, const void *B, void *C,
   GemmPlan *p = nullptr;
   int rc = get_plan(dev, g, &p);
   if (rc != HSTU_OK) return rc;
+  if (!p->tuned && !tune_plan(dev, p, A, B, C, ws, s))
+    return fail(HSTU_EHIP, "GEMM algorithm timing failed (%s)", name);
   const float alpha = 1.0f, beta = 0.0f;
   prof::Scope ps(name, s);
   hipblasStatus_t st = hipblasLtMatmul(g_blas[dev].handle, p->op, &alpha, B,
