@@ -125,7 +125,7 @@ hipEvent_t take_event() {
 }  // namespace
 
 Scope::Scope(const char *n, hipStream_t st) : name(n), s(st) {
-  if (!on.load(std::memory_order_relaxed)) return;
+  if (!n || !on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lock(mu);
   a = take_event();
   if (a && hipEventRecord(a, s) != hipSuccess) {

@@ -159,6 +159,10 @@ hipError_t launch_silu_split(const void *h, void *z, int64_t T, int32_t C,
 hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
                               int64_t T, int32_t C, int dev, hipStream_t s);
 // Zero `bytes` (a multiple of 4) of device memory with a kernel.
+// out (bf16, n elements, n % 4 == 0) = sum of `parts` float32 arrays of n
+// elements stored back to back at `part`.
+hipError_t launch_sum_parts(const float *part, void *out, int64_t n, int32_t parts, int dev,
+                            hipStream_t s);
 hipError_t launch_zero(void *p, size_t bytes, int dev, hipStream_t s);
 
 // Persistent-grid sizes (work-groups) of the bf16 attention kernels.

@@ -29,13 +29,18 @@ int blas_fail(hipblasStatus_t st, const char *what) {
   return fail(HSTU_EHIP, "hipBLASLt %s failed (status %d)", what, (int)st);
 }
 
-// Row-major C[M][N] (ldc) = op(A)[M][K] . op(B)[K][N], bf16.
+// Row-major C[M][N] (ldc) = op(A)[M][K] . op(B)[K][N], A and B bf16, C bf16
+// or (c32) float32; `batch` products at element strides sa, sb, sc.
 struct GemmShape {
   bool ta, tb;
   int64_t M, N, K, lda, ldb, ldc;
+  int32_t batch = 1;
+  int64_t sa = 0, sb = 0, sc = 0;
+  bool c32 = false;
   bool operator<(const GemmShape &o) const {
-    return std::tie(ta, tb, M, N, K, lda, ldb, ldc) <
-           std::tie(o.ta, o.tb, o.M, o.N, o.K, o.lda, o.ldb, o.ldc);
+    return std::tie(ta, tb, M, N, K, lda, ldb, ldc, batch, sa, sb, sc, c32) <
+           std::tie(o.ta, o.tb, o.M, o.N, o.K, o.lda, o.ldb, o.ldc, o.batch, o.sa, o.sb,
+                    o.sc, o.c32);
   }
 };
 
@@ -107,7 +112,19 @@ int get_plan(int dev, const GemmShape &g, GemmPlan **out) {
     st = hipblasLtMatrixLayoutCreate(&p.lb, HIP_R_16BF, g.ta ? g.M : g.K,
                                      g.ta ? g.K : g.M, g.lda);
   if (st == HIPBLAS_STATUS_SUCCESS)
-    st = hipblasLtMatrixLayoutCreate(&p.lc, HIP_R_16BF, g.N, g.M, g.ldc);
+    st = hipblasLtMatrixLayoutCreate(&p.lc, g.c32 ? HIP_R_32F : HIP_R_16BF, g.N, g.M, g.ldc);
+  if (g.batch > 1) {
+    const int32_t n = g.batch;
+    const hipblasLtMatrixLayout_t lay[3] = {p.la, p.lb, p.lc};
+    const int64_t stride[3] = {g.sb, g.sa, g.sc};
+    for (int i = 0; i < 3 && st == HIPBLAS_STATUS_SUCCESS; ++i) {
+      st = hipblasLtMatrixLayoutSetAttribute(lay[i], HIPBLASLT_MATRIX_LAYOUT_BATCH_COUNT, &n,
+                                             sizeof(n));
+      if (st == HIPBLAS_STATUS_SUCCESS)
+        st = hipblasLtMatrixLayoutSetAttribute(
+            lay[i], HIPBLASLT_MATRIX_LAYOUT_STRIDED_BATCH_OFFSET, &stride[i], sizeof(int64_t));
+    }
+  }
   if (st != HIPBLAS_STATUS_SUCCESS) {
     destroy(p);
     return blas_fail(st, "descriptor creation");
@@ -192,7 +209,8 @@ bool tune_plan(int dev, GemmPlan *p, const void *A, const void *B, void *C, void
   return true;
 }
 
-// Row-major C = op(A) . op(B) on `s`; `ws` holds GEMM_WS_BYTES.
+// Row-major C = op(A) . op(B) on `s`; `ws` holds GEMM_WS_BYTES.  `name`
+// labels the profiler scope (none when NULL).
 int gemm(int dev, const GemmShape &g, const void *A, const void *B, void *C,
          void *ws, hipStream_t s, const char *name) {
   std::lock_guard<std::mutex> lock(g_blas_mu);
@@ -200,13 +218,13 @@ int gemm(int dev, const GemmShape &g, const void *A, const void *B, void *C,
   int rc = get_plan(dev, g, &p);
   if (rc != HSTU_OK) return rc;
   if (!p->tuned && !tune_plan(dev, p, A, B, C, ws, s))
-    return fail(HSTU_EHIP, "GEMM algorithm timing failed (%s)", name);
+    return fail(HSTU_EHIP, "GEMM algorithm timing failed (%s)", name ? name : "split part");
   const float alpha = 1.0f, beta = 0.0f;
   prof::Scope ps(name, s);
   hipblasStatus_t st = hipblasLtMatmul(g_blas[dev].handle, p->op, &alpha, B,
                                        p->la, A, p->lb, &beta, C, p->lc, C,
                                        p->lc, &p->algo, ws, GEMM_WS_BYTES, s);
-  if (st != HIPBLAS_STATUS_SUCCESS) return blas_fail(st, name);
+  if (st != HIPBLAS_STATUS_SUCCESS) return blas_fail(st, name ? name : "split part");
   return HSTU_OK;
 }
 
@@ -215,12 +233,58 @@ GemmShape rm(bool ta, bool tb, int64_t M, int64_t N, int64_t K, int64_t lda,
   return GemmShape{ta, tb, M, N, K, lda, ldb, ldc};
 }
 
+// Weight gradients (K = T, small M x N) as split-K products: `parts`
+// float32 partials of M x N, summed into the bf16 result.
+constexpr int64_t SPLITK_MIN_ROWS = 1024;   // rows of T per part, at least
+int splitk_parts(int64_t M, int64_t N, int64_t T) {
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int64_t s = std::min<int64_t>(16, std::max<int64_t>(1, 256 / std::max<int64_t>(tiles, 1)));
+  while (s > 1 && T / s < SPLITK_MIN_ROWS) s /= 2;
+  return (int)s;
+}
+// float32 partials of one split-K product (a remainder part included).
+size_t splitk_bytes(int64_t M, int64_t N, int64_t T) {
+  const int s = splitk_parts(M, N, T);
+  return s > 1 ? sizeof(float) * (size_t)(M * N) * (size_t)(s + 1) : 0;
+}
+
+// Row-major C[M][N] (bf16, ldc = N) = A^T B with A [T][M] (lda) and B
+// [T][N] (ldb) bf16: for `parts` > 1, `parts` equal row blocks of T as one
+// strided batch of float32 products into `part`, the remaining rows as one
+// more, then their sum.  `name` labels the whole operation.
+int gemm_wgrad(int dev, int64_t M, int64_t N, int64_t T, const void *A, int64_t lda,
+               const void *B, int64_t ldb, void *C, float *part, void *ws, hipStream_t s,
+               const char *name) {
+  const int parts = splitk_parts(M, N, T);
+  if (parts <= 1) return gemm(dev, rm(true, false, M, N, T, lda, ldb, N), A, B, C, ws, s, name);
+  prof::Scope ps(name, s);
+  const int64_t rows = T / parts, rest = T - rows * parts;
+  GemmShape g = rm(true, false, M, N, rows, lda, ldb, N);
+  g.batch = parts;
+  g.sa = rows * lda;
+  g.sb = rows * ldb;
+  g.sc = M * N;
+  g.c32 = true;
+  int rc = gemm(dev, g, A, B, part, ws, s, nullptr);
+  if (rc != HSTU_OK) return rc;
+  if (rest > 0) {
+    GemmShape r = rm(true, false, M, N, rest, lda, ldb, N);
+    r.c32 = true;
+    rc = gemm(dev, r, (const char *)A + 2 * rows * parts * lda,
+              (const char *)B + 2 * rows * parts * ldb, part + (size_t)parts * M * N, ws, s,
+              nullptr);
+    if (rc != HSTU_OK) return rc;
+  }
+  const hipError_t e = launch_sum_parts(part, C, M * N, parts + (rest > 0 ? 1 : 0), dev, s);
+  return e == hipSuccess ? HSTU_OK : hip_fail(e, "split-K sum launch");
+}
+
 struct LayerLayout {
-  size_t attn, gemm, dy, dz, dh, total;
+  size_t attn, gemm, dy, dz, dh, part, total;
   size_t attn_bytes;
 };
 
-LayerLayout layer_layout(const Problem &p, bool for_bwd, int dev) {
+LayerLayout layer_layout(const Problem &p, int64_t D, bool for_bwd, int dev) {
   LayerLayout L{};
   size_t at = 0;
   auto take = [&](size_t bytes) {
@@ -236,6 +300,8 @@ LayerLayout layer_layout(const Problem &p, bool for_bwd, int dev) {
     L.dy = take(2 * (size_t)p.T * C);
     L.dz = take(2 * 4 * (size_t)p.T * C);
     L.dh = take(2 * 4 * (size_t)p.T * C);
+    // dW2 [C][D] and dW1 [D][4C] run one after the other: one partial area
+    L.part = take(std::max(splitk_bytes(C, D, p.T), splitk_bytes(D, 4 * C, p.T)));
   }
   L.total = at;
   return L;
@@ -276,7 +342,7 @@ size_t hstu_layer_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
     return 0;
   int dev = 0;
   if (current_device(&dev) != HSTU_OK) return 0;
-  return layer_layout(p, for_bwd != 0, dev).total;
+  return layer_layout(p, d_model, for_bwd != 0, dev).total;
 }
 
 int hstu_layer_fwd(const void *x, const void *w1, const void *w2,
@@ -296,7 +362,7 @@ int hstu_layer_fwd(const void *x, const void *w1, const void *w2,
   if (T == 0) return HSTU_OK;
   int dev = 0;
   if ((rc = current_device(&dev)) != HSTU_OK) return rc;
-  const LayerLayout L = layer_layout(p, false, dev);
+  const LayerLayout L = layer_layout(p, d_model, false, dev);
   if ((rc = check_workspace_bytes(L.total, out->workspace, out->workspace_bytes)) != HSTU_OK)
     return rc;
   hipStream_t s = (hipStream_t)stream;
@@ -346,7 +412,7 @@ int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
     return fail(HSTU_EINVAL, "rab->time_w given but io->d_time_w is NULL");
   int dev = 0;
   if ((rc = current_device(&dev)) != HSTU_OK) return rc;
-  const LayerLayout L = layer_layout(p, true, dev);
+  const LayerLayout L = layer_layout(p, d_model, true, dev);
   if ((rc = check_workspace_bytes(L.total, io->workspace, io->workspace_bytes)) != HSTU_OK)
     return rc;
   hipStream_t s = (hipStream_t)stream;
@@ -367,8 +433,8 @@ int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
     if ((rc = gemm(dev, rm(false, true, T, C, D, D, D, C), io->dout, w2,
                    ws + L.dy, ws + L.gemm, s, "gemm_dy")) != HSTU_OK)
       return rc;
-    if ((rc = gemm(dev, rm(true, false, C, D, T, C, D, D), io->y, io->dout,
-                   io->dw2, ws + L.gemm, s, "gemm_dw2")) != HSTU_OK)
+    if ((rc = gemm_wgrad(dev, C, D, T, io->y, C, io->dout, D, io->dw2,
+                         (float *)(ws + L.part), ws + L.gemm, s, "gemm_dw2")) != HSTU_OK)
       return rc;
   }
   // Attention backward into the dz planes (du, dv, dq, dk); also writes the
@@ -388,8 +454,8 @@ int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
   if ((rc = gemm(dev, rm(false, true, T, D, 4 * C, 4 * C, 4 * C, D), ws + L.dh,
                  w1, io->dx, ws + L.gemm, s, "gemm_dx")) != HSTU_OK)
     return rc;
-  return gemm(dev, rm(true, false, D, 4 * C, T, D, 4 * C, 4 * C), x, ws + L.dh,
-              io->dw1, ws + L.gemm, s, "gemm_dw1");
+  return gemm_wgrad(dev, D, 4 * C, T, x, D, ws + L.dh, 4 * C, io->dw1,
+                    (float *)(ws + L.part), ws + L.gemm, s, "gemm_dw1");
 }
 
 }  // extern "C"

@@ -1,6 +1,7 @@
 // Pointwise kernels of the HSTU layer shell: the SiLU + column split that
 // turns f1's output into the attention's U, V, Q, K planes, its derivative
-// + merge on the way back, and a zero fill.
+// + merge on the way back, the sum of split-K partial products, and a zero
+// fill.
 //
 // Both main kernels are pure streaming passes (HBM-bound): each thread moves
 // 16-byte chunks of eight bf16, a chunk never straddles two planes (the
@@ -86,6 +87,22 @@ dsilu_merge_kernel(const uint4 *__restrict__ h, const uint4 *__restrict__ dz,
   }
 }
 
+// out[x] = bf16(sum_{s < parts} part[s][x]) for x < n (n % 4 == 0), summed
+// in the order s = 0, 1, ...
+__global__ void __launch_bounds__(PW_THREADS)
+sum_parts_kernel(const float4 *__restrict__ part, uint2 *__restrict__ out, int64_t n4,
+                 int32_t parts) {
+  const int64_t stride = (int64_t)gridDim.x * PW_THREADS;
+  for (int64_t x = (int64_t)blockIdx.x * PW_THREADS + threadIdx.x; x < n4; x += stride) {
+    float4 a = part[x];
+    for (int32_t p = 1; p < parts; ++p) {
+      const float4 b = part[(int64_t)p * n4 + x];
+      a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    }
+    out[x] = make_uint2(pack2(a.x, a.y), pack2(a.z, a.w));
+  }
+}
+
 __global__ void __launch_bounds__(PW_THREADS)
 zero_kernel(uint32_t *__restrict__ p, int64_t words) {
   const int64_t stride = (int64_t)gridDim.x * PW_THREADS;
@@ -121,6 +138,15 @@ hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
                      dim3(PW_THREADS), 0, s, (const uint4 *)h,
                      (const uint4 *)dz, (uint4 *)dh, chunks, 4 * C / 8, C / 8,
                      T * (int64_t)C / 8);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_parts(const float *part, void *out, int64_t n, int32_t parts, int dev,
+                            hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (n4 == 0) return hipSuccess;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(pw_grid(n4, dev)), dim3(PW_THREADS), 0, s,
+                     (const float4 *)part, (uint2 *)out, n4, parts);
   return hipGetLastError();
 }
 

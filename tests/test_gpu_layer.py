@@ -82,6 +82,17 @@ def test_layer_small(case):
     compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
 
 
+def test_layer_split_k_weight_gradients():
+    """Enough tokens (T = 2 x 1050 + 1) that dW1 and dW2 run as split-K
+    products (two row blocks in one strided batch plus a one-row
+    remainder), checked in full against the oracle."""
+    lengths = [700, 700, 701]
+    say(f"layer split-K: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=1, d=64, N=704, seed=320, layer_dim=64)
+    got = run_layer(w)
+    compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
+
+
 def test_layer_workload4_sampled():
     w = inputs.workload(4)
     say(f"layer workload {w.name}: T={w.T} pairs/head={w.pairs} (full-size GPU run)")
