@@ -284,23 +284,27 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
     const int h = blockIdx.x / chunks;
     const int m = (blockIdx.x % chunks) * 64 + lane;
     if (m < N) {
-      // four sequences per step, loads issued together (no dependent chain)
-      float a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      // eight sequences per step: their records, then their partials, each
+      // group of loads issued together (two memory latencies per step)
+      constexpr int G = 8;
+      float part[G];
+#pragma unroll
+      for (int k = 0; k < G; ++k) part[k] = 0.0f;
       int b = wv;
-      for (; b + 3 * FIN_WAVES < B; b += 4 * FIN_WAVES) {
-        const SeqInfo s0 = info[b], s1 = info[b + FIN_WAVES];
-        const SeqInfo s2 = info[b + 2 * FIN_WAVES], s3 = info[b + 3 * FIN_WAVES];
-        const float v0 = s0.len > m ? pos_part[(s0.start + m) * H + h] : 0.0f;
-        const float v1 = s1.len > m ? pos_part[(s1.start + m) * H + h] : 0.0f;
-        const float v2 = s2.len > m ? pos_part[(s2.start + m) * H + h] : 0.0f;
-        const float v3 = s3.len > m ? pos_part[(s3.start + m) * H + h] : 0.0f;
-        acc += v0; a1 += v1; a2 += v2; a3 += v3;
+      for (; b + (G - 1) * FIN_WAVES < B; b += G * FIN_WAVES) {
+        SeqInfo si[G];
+#pragma unroll
+        for (int k = 0; k < G; ++k) si[k] = info[b + k * FIN_WAVES];
+#pragma unroll
+        for (int k = 0; k < G; ++k)
+          part[k] += si[k].len > m ? pos_part[(si[k].start + m) * H + h] : 0.0f;
       }
       for (; b < B; b += FIN_WAVES) {
         const SeqInfo si = info[b];
         if (si.len > m) acc += pos_part[(si.start + m) * H + h];
       }
-      acc += (a1 + a2) + a3;
+#pragma unroll
+      for (int k = 0; k < G; ++k) acc += part[k];
     }
     red[wv][lane] = acc;
     __syncthreads();
