@@ -621,23 +621,24 @@ struct StreamSmem {
   int item;
 };
 
-// Per-lane running sum of d_time contributions over one time index (the
-// lane's pairs visit non-decreasing indices when timestamps are ordered, so
-// a run is flushed only when its index changes).  A run is opened by the
-// first index of the item's first tile (start), so adding needs no test for
-// an empty run.
+// Per-lane running sum of d_time contributions over one float-exponent time
+// index (the lane's pairs visit non-decreasing indices when timestamps are
+// ordered, so a run ends only when its index changes); a finished run goes
+// to its bucket of the work-group's histogram `hist`.  A run is opened by
+// the first index of the item's first tile (start), so adding needs no test
+// for an empty run.
 struct TimeRun {
   float sum = 0.0f;
   int cur = -1;
   __device__ __forceinline__ void start(int k) { cur = cur < 0 ? k : cur; }
-  __device__ __forceinline__ void add(double *acc, int k, float v) {
+  __device__ __forceinline__ void add(double *hist, int nb, int k, float v) {
     const bool change = k != cur;
-    if (change) atomicAdd(&acc[cur], (double)sum);
+    if (change) atomicAdd(&hist[bucket_of_index(cur, nb)], (double)sum);
     sum = change ? v : sum + v;
     cur = k;
   }
-  __device__ __forceinline__ void flush(double *acc) {
-    if (cur >= 0) atomicAdd(&acc[cur], (double)sum);
+  __device__ __forceinline__ void flush(double *hist, int nb) {
+    if (cur >= 0) atomicAdd(&hist[bucket_of_index(cur, nb)], (double)sum);
     cur = -1;
     sum = 0.0f;
   }
@@ -852,7 +853,6 @@ template <int D, bool POS>
 struct DkvSmem {
   StreamSmem<D> s;
   double pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
-  double kacc[KTAB];            // this item's d_time by float-exponent index
   // At d=64 the item's stationary K and V tiles live here (swizzled, filled
   // by global-to-LDS loads) instead of in registers, which lets the kernel
   // run three waves per SIMD.
@@ -1085,7 +1085,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
           if (!slow) {
             if (hh == 0) run.start(tk[0]);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) run.add(smx.kacc, tk[e], dsv[e]);
+            for (int e = 0; e < 8; ++e) run.add(my_t, P.nb, tk[e], dsv[e]);
           } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -1116,23 +1116,13 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       }
     }
 
-    // sum the two query halves, store dK, dV (bf16); fold this item's
-    // d_time by index into the work-group histogram
-    if (TIME) run.flush(smx.kacc);
+    // close the d_time runs; sum the two query halves, store dK, dV (bf16)
+    if (TIME) run.flush(my_t, P.nb);
     lds_barrier();
     if constexpr (POS) {   // every diagonal of the last window is final
       if (tid < 2 * TILE - 1)
         dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid,
                     si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
-    }
-    if (TIME) {
-      for (int x = tid; x < KTAB; x += THREADS) {
-        const double val = smx.kacc[x];
-        if (val != 0.0) {
-          smx.kacc[x] = 0.0;
-          atomicAdd(&my_t[bucket_of_index(x, P.nb)], val);
-        }
-      }
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
                       row_stride, k_valid, P.inv_n);
@@ -1141,14 +1131,13 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
 }
 
 // Work-group start of the kernels that run dK/dV items: zeroed d_time
-// histogram and index accumulators, cleared flags and d_pos windows (the
+// histogram, cleared flags and d_pos windows (the
 // time tables are staged by the first item).
 template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dkv_kernel_init(const KParams &P, DkvSmem<D, POS> &smx,
                                                 double *tacc, float *dyn, int tid0) {
   if (TIME) {
     for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
-    for (int x = tid0; x < KTAB; x += THREADS) smx.kacc[x] = 0.0;
   }
   if (tid0 < 2) smx.s.flag[tid0] = 0;
   if constexpr (POS)
