@@ -54,6 +54,7 @@ namespace {
 
 constexpr int THREADS = 256;     // 4 waves
 constexpr int RM_PAD = 8;        // backward: row-major LDS stride D+8 bf16
+constexpr int DS_STRIDE = TILE + RM_PAD;   // backward: staged dS^T tile
 constexpr int POS_COPY = 2 * TILE + 4;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
@@ -77,6 +78,8 @@ struct KParams {
   int32_t H, N, nb;
   float inv_n;
   int32_t all_heads;      // time tables of every head staged once per work-group
+  int32_t fuse_single;    // combined backward, d=64: one-tile sequences' dK/dV
+                          // items compute their dQ too (no dQ items)
 };
 
 // Stationary 32-row operand: lane holds row `row` of the tile (zero when
@@ -183,15 +186,37 @@ __device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, i
   return dyn;
 }
 
+// Coalesced bf16 store of a 64 x D fp32 tile in LDS: every thread converts 8
+// consecutive floats of one row, scales them by `scale` and writes them as a
+// single 16-byte chunk; rows at or beyond `valid` are not written.
+template <int D>
+__device__ __forceinline__ void store_rows(const float *red, int tid, u16 *__restrict__ out,
+                                           int row_stride, int valid, float scale) {
+  constexpr int CH = TILE * D / 8 / THREADS;
+#pragma unroll
+  for (int x = 0; x < CH; ++x) {
+    const int ch = tid + THREADS * x;
+    const int row = ch / (D / 8), c8 = ch % (D / 8);
+    if (row < valid) {
+      const float4 a = *(const float4 *)(red + row * D + 8 * c8);
+      const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
+      uint4 pk;
+      pk.x = pack2(scale * a.x, scale * a.y);
+      pk.y = pack2(scale * a.z, scale * a.w);
+      pk.z = pack2(scale * b.x, scale * b.y);
+      pk.w = pack2(scale * b.z, scale * b.w);
+      *(uint4 *)(out + row * row_stride + 8 * c8) = pk;
+    }
+  }
+}
+
 // Cross-wave sum of a 64 x D fp32 output tile and its coalesced bf16 store.
 // The two waves of each stationary row half hold partial sums over the two
 // halves of the streamed side, in accumulator layout (rows 32*half +
 // c_row(r, g), columns 32*db + l32).  The writer wave stores its blocks to
-// LDS, its partner adds its own in place, then every thread converts 8
-// consecutive floats of one
-// row, scales them by `scale` and writes them as a single 16-byte chunk;
-// rows at or beyond `valid` are not written.  (The partner reads, adds and writes back its own
-// addresses: LDS float atomics are far slower here even without conflicts.)
+// LDS, its partner adds its own in place, then store_rows writes the tile.
+// (The partner reads, adds and writes back its own addresses: LDS float
+// atomics are far slower here even without conflicts.)
 template <int D>
 __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D / 32],
                                                bool writer, int half, int g, int l32,
@@ -214,22 +239,22 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
         red[(32 * half + c_row(r, g)) * D + 32 * db + l32] += acc[db][r];
   }
   lds_barrier();
-  constexpr int CH = TILE * D / 8 / THREADS;
+  store_rows<D>(red, tid, out, row_stride, valid, scale);
+}
+
+// Store of a 64 x D fp32 output tile whose 32 x 32 blocks are held by one
+// wave each: wave (half, cb) holds rows 32*half + c_row(r, g), columns
+// 32*cb + l32 (D = 64: the four waves cover the tile).
+template <int D>
+__device__ __forceinline__ void quad_store_tile(float *red, const f32x16 &acc, int half, int cb,
+                                                int g, int l32, int tid, u16 *__restrict__ out,
+                                                int row_stride, int valid, float scale) {
+  static_assert(D == 64, "four 32 x 32 blocks");
+  lds_barrier();
 #pragma unroll
-  for (int x = 0; x < CH; ++x) {
-    const int ch = tid + THREADS * x;
-    const int row = ch / (D / 8), c8 = ch % (D / 8);
-    if (row < valid) {
-      const float4 a = *(const float4 *)(red + row * D + 8 * c8);
-      const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
-      uint4 pk;
-      pk.x = pack2(scale * a.x, scale * a.y);
-      pk.y = pack2(scale * a.z, scale * a.w);
-      pk.z = pack2(scale * b.x, scale * b.y);
-      pk.w = pack2(scale * b.z, scale * b.w);
-      *(uint4 *)(out + row * row_stride + 8 * c8) = pk;
-    }
-  }
+  for (int r = 0; r < 16; ++r) red[(32 * half + c_row(r, g)) * D + 32 * cb + l32] = acc[r];
+  lds_barrier();
+  store_rows<D>(red, tid, out, row_stride, valid, scale);
 }
 
 // ------------------------------------------------- swizzled DMA-fed tiles
@@ -888,7 +913,7 @@ template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx, float *dyn,
                                          double *tacc, const int tid0, const WorkEntry e,
                                          const int h, int &phase, float *&pend_p,
-                                         float &pend_v, int &nxt) {
+                                         float &pend_v, int &nxt, u16 *dsb = nullptr) {
   constexpr int ST = D + RM_PAD;
   StreamSmem<D> &sm = smx.s;
     int tid = tid0;
@@ -910,6 +935,10 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     // key tile's diagonal step, where the causal mask removes them, and
     // query rows past the sequence carry dO = 0
     constexpr bool KV_LDS = D == 64;
+    // A one-tile sequence has a single tile pair: with `dsb` given, this item
+    // also computes its dQ = dS K, from dS^T staged in `dsb` ([key][query],
+    // stride DS_STRIDE) and the stationary K tile.
+    const bool with_dq = KV_LDS && dsb != nullptr && si.ntiles == 1;
     bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
     if constexpr (KV_LDS) {
       dma_tile<D>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
@@ -1108,6 +1137,12 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         pd.w = pack2(dsv[6], dsv[7]);
         const bf16x8 a8 = as_bf16x8(pa), d8 = as_bf16x8(pd);
         const int krow = 32 * wi + 16 * hh + 4 * g;
+        if (with_dq) {
+          // this lane's key row; its 8 queries are krow .. +3 and krow+8 .. +11
+          u16 *row = dsb + j_loc * DS_STRIDE + krow;
+          *(uint2 *)row = make_uint2(pd.x, pd.y);
+          *(uint2 *)(row + 8) = make_uint2(pd.z, pd.w);
+        }
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
           dv[db] = mfma32(a8, read_tr(sm.t.b, ST, krow, 32 * db, lane), dv[db]);
@@ -1123,6 +1158,21 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       if (tid < 2 * TILE - 1)
         dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid,
                     si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
+    }
+    if constexpr (KV_LDS) {
+      if (with_dq) {
+        // dQ block (query half wi, columns 32 wj ..): dS rows read transposed
+        // out of dsb, K columns out of the stationary tile, all 64 keys
+        f32x16 dq;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dq[r] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < TILE / 16; ++kk)
+          dq = mfma32(read_tr(dsb, DS_STRIDE, 16 * kk + 4 * g, 32 * wi, lane),
+                      sread_tr<D>(smx.kst, 16 * kk + 4 * g, 32 * wj, lane), dq);
+        quad_store_tile<D>(&sm.red[0][0], dq, wi, wj, g, l32, tid, P.dq_out + koff,
+                           row_stride, k_valid, P.inv_n);
+      }
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
                       row_stride, k_valid, P.inv_n);
@@ -1167,13 +1217,15 @@ template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_bwd_kernel(KParams P) {
   __shared__ DkvSmem<D, POS> smx;
+  // dS^T of a one-tile sequence's tile pair (d=64, see dkv_item)
+  __shared__ __attribute__((aligned(16))) u16 dsb[D == 64 ? TILE * DS_STRIDE : 8];
   StreamSmem<D> &sm = smx.s;
   // dynamic LDS: [H][nb] d_time (double), then the time tables
   extern __shared__ double dyn_k[];
   double *tacc = dyn_k;
   float *dyn = (float *)(dyn_k + P.H * P.nb);
   const int tid0 = threadIdx.x;
-  const int n_items = 2 * P.ctrl[CTRL_N_ENTRIES] * P.H;
+  const int n_items = P.ctrl[CTRL_N_BWD] * P.H;
   dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
   lds_barrier();
   int phase = 0;
@@ -1187,7 +1239,8 @@ attn_bwd_kernel(KParams P) {
       e.tile &= ~BWD_DQ_FLAG;
       dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase, nxt);
     } else {
-      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt);
+      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt,
+                             P.fuse_single ? dsb : nullptr);
     }
   }
   dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
@@ -1359,6 +1412,8 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
     P.dq_out = (u16 *)dq;
     P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
     P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
+    // must match the scheduler's choice (sched_args)
+    P.fuse_single = p.d == 64 ? 1 : 0;
     HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
                   hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_both), dim3(THREADS),
                                      k_dyn_bytes(p), s, P));

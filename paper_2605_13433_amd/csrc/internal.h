@@ -30,6 +30,7 @@ enum CtrlSlot {
   CTRL_POP_DQ = 2,      // pop counter of the dQ kernel
   CTRL_POP_DKV = 3,     // pop counter of the dK/dV kernel (and fp32 pass)
   CTRL_POP_BWD = 4,     // pop counter of the combined bf16 backward kernel
+  CTRL_N_BWD = 5,       // entries in the combined backward list
   CTRL_WORDS = 64
 };
 

@@ -50,6 +50,7 @@ SMALL = [
     ([100, 33, 0, 7], 1, 128, 128, False, True),
     ([77, 250, 3], 2, 64, 250, False, False),
     ([2, 1, 1, 3, 64], 4, 64, 64, True, True),
+    ([1, 40, 64, 90, 5, 0], 2, 64, 128, False, True),   # one-tile sequences, time bias only
 ]
 
 
