@@ -78,8 +78,8 @@ struct KParams {
   int32_t H, N, nb;
   float inv_n;
   int32_t all_heads;      // time tables of every head staged once per work-group
-  int32_t fuse_single;    // combined backward, d=64: one-tile sequences' dK/dV
-                          // items compute their dQ too (no dQ items)
+  int32_t fuse_dq0;       // combined backward, d=64: the dK/dV items of first
+                          // k-tiles compute their q-tile's dQ (no such dQ items)
 };
 
 // Stationary 32-row operand: lane holds row `row` of the tile (zero when
@@ -906,6 +906,22 @@ __device__ __forceinline__ void dpos_retire(double (*prev)[2 * TILE], double (*c
   }
 }
 
+// dQ block (query half wi, columns 32 wj ..) of a sequence's first q-tile
+// at d=64: its tile pair's dS read transposed out of dsb, K columns out of
+// the stationary K tile, all 64 keys.
+template <int D>
+__device__ __forceinline__ f32x16 dq0_block(const u16 *dsb, const u16 *kst, int wi, int wj, int g,
+                                            int lane) {
+  f32x16 dq;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dq[r] = 0.0f;
+#pragma unroll
+  for (int kk = 0; kk < TILE / 16; ++kk)
+    dq = mfma32(read_tr(dsb, DS_STRIDE, 16 * kk + 4 * g, 32 * wi, lane),
+                sread_tr<D>(kst, 16 * kk + 4 * g, 32 * wj, lane), dq);
+  return dq;
+}
+
 // One k-stationary item: dV_j, dK_j for a 64-row key tile of one head over
 // its query tiles, with the table gradients (d_pos through the sheared tile
 // and the rolling diagonal window, d_time through per-lane index runs).
@@ -935,10 +951,11 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     // key tile's diagonal step, where the causal mask removes them, and
     // query rows past the sequence carry dO = 0
     constexpr bool KV_LDS = D == 64;
-    // A one-tile sequence has a single tile pair: with `dsb` given, this item
-    // also computes its dQ = dS K, from dS^T staged in `dsb` ([key][query],
-    // stride DS_STRIDE) and the stationary K tile.
-    const bool with_dq = KV_LDS && dsb != nullptr && si.ntiles == 1;
+    // dQ of a sequence's first q-tile comes from its tile pair (0, 0) alone:
+    // with `dsb` given, the item of k-tile 0 stages that pair's dS^T in
+    // `dsb` ([key][query], stride DS_STRIDE) and computes dQ = dS K against
+    // the stationary K tile at the item's end (both stay untouched until then).
+    const bool with_dq = KV_LDS && dsb != nullptr && kt == 0;
     bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
     if constexpr (KV_LDS) {
       dma_tile<D>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
@@ -1137,7 +1154,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         pd.w = pack2(dsv[6], dsv[7]);
         const bf16x8 a8 = as_bf16x8(pa), d8 = as_bf16x8(pd);
         const int krow = 32 * wi + 16 * hh + 4 * g;
-        if (with_dq) {
+        if (with_dq && qt == kt) {
           // this lane's key row; its 8 queries are krow .. +3 and krow+8 .. +11
           u16 *row = dsb + j_loc * DS_STRIDE + krow;
           *(uint2 *)row = make_uint2(pd.x, pd.y);
@@ -1160,19 +1177,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
                     si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
     }
     if constexpr (KV_LDS) {
-      if (with_dq) {
-        // dQ block (query half wi, columns 32 wj ..): dS rows read transposed
-        // out of dsb, K columns out of the stationary tile, all 64 keys
-        f32x16 dq;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) dq[r] = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < TILE / 16; ++kk)
-          dq = mfma32(read_tr(dsb, DS_STRIDE, 16 * kk + 4 * g, 32 * wi, lane),
-                      sread_tr<D>(smx.kst, 16 * kk + 4 * g, 32 * wj, lane), dq);
-        quad_store_tile<D>(&sm.red[0][0], dq, wi, wj, g, l32, tid, P.dq_out + koff,
-                           row_stride, k_valid, P.inv_n);
-      }
+      if (with_dq)
+        quad_store_tile<D>(&sm.red[0][0], dq0_block<D>(dsb, smx.kst, wi, wj, g, lane), wi, wj,
+                           g, l32, tid, P.dq_out + koff, row_stride, k_valid, P.inv_n);
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
                       row_stride, k_valid, P.inv_n);
@@ -1217,7 +1224,7 @@ template <int D, bool POS, bool TIME>
 __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_bwd_kernel(KParams P) {
   __shared__ DkvSmem<D, POS> smx;
-  // dS^T of a one-tile sequence's tile pair (d=64, see dkv_item)
+  // dS^T of a first tile pair (d=64, see dkv_item)
   __shared__ __attribute__((aligned(16))) u16 dsb[D == 64 ? TILE * DS_STRIDE : 8];
   StreamSmem<D> &sm = smx.s;
   // dynamic LDS: [H][nb] d_time (double), then the time tables
@@ -1240,7 +1247,7 @@ attn_bwd_kernel(KParams P) {
       dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase, nxt);
     } else {
       dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt,
-                             P.fuse_single ? dsb : nullptr);
+                             P.fuse_dq0 ? dsb : nullptr);
     }
   }
   dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
@@ -1413,7 +1420,7 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
     P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
     P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
     // must match the scheduler's choice (sched_args)
-    P.fuse_single = p.d == 64 ? 1 : 0;
+    P.fuse_dq0 = p.d == 64 ? 1 : 0;
     HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
                   hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_both), dim3(THREADS),
                                      k_dyn_bytes(p), s, P));

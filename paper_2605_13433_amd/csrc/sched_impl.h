@@ -17,10 +17,11 @@
 //     dK/dV kernels.
 //   * combined backward list: both kinds, dK/dV entries before dQ entries of
 //     equal cost (dQ entries flagged), consumed by the combined bf16
-//     backward kernel.  With `fuse_single` set, sequences of one tile get no
-//     dQ entry (their dK/dV item computes dQ as well); those entries would
-//     be the list's last ones in either order, so the list just ends
-//     earlier.
+//     backward kernel.  With `fuse_dq0` set, no sequence gets a dQ entry for
+//     its first q-tile (the dK/dV item of its first k-tile computes it); in
+//     cost-major order those entries would be the list's last ones, in
+//     sequence-major order the last one of each sequence's run, so the
+//     list is one entry per sequence shorter.
 //
 // Two orders, chosen on the device per call:
 //   * cost-major: entries sorted by cost, longest first -- the makespan
@@ -69,7 +70,7 @@ struct SchedArgs {
   int32_t nbins, cap;
   int32_t H;
   int32_t grid_hint;                  // nominal persistent work-groups
-  int32_t fuse_single;                // no dQ entries for one-tile sequences
+  int32_t fuse_dq0;                   // no dQ entries for first q-tiles
   float *zero_out;
   int32_t n_zero;
 };
@@ -130,10 +131,9 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     a.ctrl[CTRL_POP_DQ] = 0;
     a.ctrl[CTRL_POP_DKV] = 0;
     a.ctrl[CTRL_POP_BWD] = 0;
-    // cost-major: the one-tile sequences' dQ entries are the last count[1]
-    // slots (cost 1, highest ranks); sequence-major: those sequences come
-    // last and keep only their dK/dV entries
-    const int32_t n_bwd = 2 * sm.total - (a.fuse_single ? sm.count[1] : 0);
+    // every non-empty sequence (sm.rank0[1] + sm.count[1] of them) has one
+    // first q-tile
+    const int32_t n_bwd = 2 * sm.total - (a.fuse_dq0 ? sm.rank0[1] + sm.count[1] : 0);
     a.ctrl[CTRL_N_BWD] = n_bwd < 2 * a.cap ? n_bwd : 2 * a.cap;
   }
   __syncthreads();
@@ -162,14 +162,14 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
         // dK/dV then the dQ entry of each cost, from nt down to 1
         WorkEntry wq = we;
         wq.tile |= BWD_DQ_FLAG;
-        const bool single = a.fuse_single && nt == 1;
-        const int bk = single && seq_major ? 2 * sm.sstart[1] + (r - sm.rank0[1])
-                       : seq_major ? 2 * base + 2 * t
-                                   : 2 * sm.cstart[ck] + r;
-        const int bq = seq_major ? 2 * base + 2 * (nt - 1 - t) + 1
+        // sequence-major with fuse_dq0: each earlier sequence's run is one
+        // entry shorter (its first q-tile's dQ entry, the run's last, is gone)
+        const int run0 = 2 * base - (a.fuse_dq0 ? r : 0);
+        const int bk = seq_major ? run0 + 2 * t : 2 * sm.cstart[ck] + r;
+        const int bq = seq_major ? run0 + 2 * (nt - 1 - t) + 1
                                  : 2 * sm.cstart[cq] + sm.rank0[cq] + sm.count[cq] + r;
         if (bk < 2 * a.cap) a.list_b[bk] = we;
-        if (!single && bq < 2 * a.cap) a.list_b[bq] = wq;
+        if (!(a.fuse_dq0 && t == 0) && bq < 2 * a.cap) a.list_b[bq] = wq;
       }
     }
   }
@@ -192,7 +192,7 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.cap = (int32_t)p.max_entries;
   a.H = p.H;
   a.grid_hint = 4 * L.num_cu;
-  a.fuse_single = L.list_b && L.bwd_combined && p.d == 64 ? 1 : 0;
+  a.fuse_dq0 = L.list_b && L.bwd_combined && p.d == 64 ? 1 : 0;
   a.zero_out = L.dtime_part ? (float *)(base + L.dtime_part) : nullptr;
   a.n_zero = L.dtime_part ? DTIME_BINS * p.H * p.nb : 0;
   return a;
