@@ -55,6 +55,7 @@ namespace {
 constexpr int THREADS = 256;     // 4 waves
 constexpr int RM_PAD = 8;        // backward: row-major LDS stride D+8 bf16
 constexpr int DS_STRIDE = TILE + RM_PAD;   // backward: staged dS^T tile
+constexpr int BWD_STAGE_BATCH = 1;         // backward: time-table loads in flight per thread
 constexpr int POS_COPY = 2 * TILE + 4;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
@@ -164,25 +165,53 @@ __device__ __forceinline__ float silu2_over_n(float xs, float nl) {
 // then the nb raw buckets for the exact path.
 __device__ __forceinline__ int time_slot_floats(const KParams &P) { return KTAB + P.nb; }
 
-__device__ __forceinline__ void stage_time_head(const KParams &P, float *slot, int h, int tid,
-                                                float scale) {
-  const float *tab = P.time_w + (int64_t)h * P.nb;
-  for (int x = tid; x < KTAB; x += THREADS) slot[x] = scale * tab[bucket_of_index(x, P.nb)];
-  for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = scale * tab[x];
+// Slots of heads h0 .. h0+nh-1, back to back from `dyn`.  Each thread
+// issues the loads of BATCH entries before it stores any, so staging costs a
+// few memory latencies rather than one per entry (a smaller batch where the
+// caller's registers are scarce).
+template <int BATCH>
+__device__ __forceinline__ void stage_time_heads(const KParams &P, float *dyn, int h0, int nh,
+                                                 int tid, float scale) {
+  const int per = time_slot_floats(P);
+  if constexpr (BATCH == 1) {
+    for (int hl = 0; hl < nh; ++hl) {
+      const float *tab = P.time_w + (int64_t)(h0 + hl) * P.nb;
+      float *slot = dyn + hl * per;
+      for (int x = tid; x < KTAB; x += THREADS) slot[x] = scale * tab[bucket_of_index(x, P.nb)];
+      for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = scale * tab[x];
+    }
+    return;
+  }
+  const int total = nh * per;
+  for (int i0 = tid; i0 < total; i0 += BATCH * THREADS) {
+    float v[BATCH];
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) {
+      const int i = min(i0 + k * THREADS, total - 1);    // in bounds, used if < total
+      const int hl = i / per, x = i - hl * per;
+      const int src = x < KTAB ? bucket_of_index(x, P.nb) : x - KTAB;
+      v[k] = P.time_w[(int64_t)(h0 + hl) * P.nb + src];
+    }
+#pragma unroll
+    for (int k = 0; k < BATCH; ++k) {
+      const int i = i0 + k * THREADS;
+      if (i < total) dyn[i] = scale * v[k];
+    }
+  }
 }
 
 // Kernel start: every head's tables when they fit (then no per-item staging).
+template <int BATCH>
 __device__ __forceinline__ void stage_all_heads(const KParams &P, float *dyn, int tid,
                                                 float scale) {
-  if (!P.all_heads) return;
-  for (int h = 0; h < P.H; ++h) stage_time_head(P, dyn + h * time_slot_floats(P), h, tid, scale);
+  if (P.all_heads) stage_time_heads<BATCH>(P, dyn, 0, P.H, tid, scale);
 }
 
 // Item start: the slot of head h (staged now if tables are per item).
 __device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, int h, int tid,
                                                  float scale) {
   if (P.all_heads) return dyn + h * time_slot_floats(P);
-  stage_time_head(P, dyn, h, tid, scale);
+  stage_time_heads<1>(P, dyn, h, 1, tid, scale);
   return dyn;
 }
 
@@ -387,7 +416,6 @@ attn_fwd_kernel(KParams P) {
   if (cur >= n_items) return;
   const int tid0 = threadIdx.x;
   if (tid0 < 3) sm.flag[tid0] = 0;
-  if (TIME) stage_all_heads(P, dyn, tid0, L2E);
   int phase = 0;
 
   Item it = load_item(P, cur);
@@ -404,6 +432,8 @@ attn_fwd_kernel(KParams P) {
     load_stationary<D>(P.q + ((it.start + (int64_t)it.tile * TILE) * P.H + it.h) * D, i_loc,
                        it.len - it.tile * TILE, P.H * D, g, qreg);
   }
+  // the tables after the first item's loads: both latencies overlap
+  if (TIME) stage_all_heads<8>(P, dyn, tid0, L2E);
 
   for (;;) {
     // Lane-derived values are rebuilt per item from an opaque copy of the
@@ -749,7 +779,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     if (TIME) {
       // the work-group's tables, staged at its first item after that item's
       // loads (both latencies overlap)
-      if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);
+      if (phase == 0) stage_all_heads<BWD_STAGE_BATCH>(P, dyn, tid, 1.0f);
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
@@ -984,7 +1014,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
-      if (phase == 0) stage_all_heads(P, dyn, tid, 1.0f);   // as in dq_item
+      if (phase == 0) stage_all_heads<BWD_STAGE_BATCH>(P, dyn, tid, 1.0f);   // as in dq_item
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (float)(int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
