@@ -55,7 +55,6 @@ namespace {
 constexpr int THREADS = 256;     // 4 waves
 constexpr int RM_PAD = 8;        // backward: row-major LDS stride D+8 bf16
 constexpr int DS_STRIDE = TILE + RM_PAD;   // backward: staged dS^T tile
-constexpr int BWD_STAGE_BATCH = 1;         // backward: time-table loads in flight per thread
 constexpr int POS_COPY = 2 * TILE + 4;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
@@ -779,7 +778,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     if (TIME) {
       // the work-group's tables, staged at its first item after that item's
       // loads (both latencies overlap)
-      if (phase == 0) stage_all_heads<BWD_STAGE_BATCH>(P, dyn, tid, 1.0f);
+      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, 1.0f);
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
@@ -1014,7 +1013,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
-      if (phase == 0) stage_all_heads<BWD_STAGE_BATCH>(P, dyn, tid, 1.0f);   // as in dq_item
+      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, 1.0f);   // as in dq_item
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (float)(int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
