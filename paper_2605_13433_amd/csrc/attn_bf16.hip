@@ -11,7 +11,10 @@
 //                 (per-sequence diagonal partials for d_pos, binned
 //                 per-work-group histograms for d_time)
 //   attn_bwd_dq   q-stationary: dQ_i = sum_{j<=i} dS_ij k_j
-//   attn_bwd      both item kinds in one launch (small problems)
+//   attn_bwd      both item kinds in one launch (small problems); at d=64
+//                 the dK/dV item of k-tile 0 also produces the dQ of q-tile
+//                 0, which depends on tile pair (0, 0) alone, so the merged
+//                 list has no dQ item for any sequence's first q-tile
 //
 // With many items per work-group the two backward item kinds run as two
 // launches, each at the occupancy its own register footprint allows (the dQ
