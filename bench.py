@@ -8,13 +8,18 @@ inputs already resident in HBM.
 Headline: valid-token TFLOP/s = 12 d H P / t_step, with P = sum_b
 L_b (L_b + 1) / 2 causal pairs per head (forward 4 d H P for QK^T and AV,
 backward 8 d H P for dA, dV, dQ, dK; recompute, bias, SiLU and LayerNorm
-work are not credited; padding does not exist).  Prints one JSON line.
+work are not credited; padding does not exist), on the largest workload
+that fits one GPU: the Zipf batch (1024 sequences, lengths 1..8192, H = 4,
+d = 64, position bias).  Prints one JSON line, which also carries a
+"configs" object with every workload timed the same way (the fp32
+forward-only parity batch by its forward time), each beside its roofline
+ceiling.
 
 With the layer workload (--workload 4) the line also carries a "layer"
 object: the whole HSTU layer around the attention (f1/f2 GEMMs, SiLU split
 and their backward) timed the same way.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5]
 """
 from __future__ import annotations
 
@@ -125,6 +130,26 @@ def load_traffic(kernel: str, workload: str, sha: str):
     except (KeyError, ValueError):
         return None
     return (fetch * scale_f + write * scale_w) * 1024.0
+
+
+def load_clock(kernel: str, workload: str, sha: str):
+    """Average shader clock (MHz) during the kernel's dispatches, from the
+    committed counter summary (GRBM_GUI_ACTIVE cycles over the dispatch
+    duration), if taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha") != sha:
+        return None
+    try:
+        return float(vals["clock_mhz"])
+    except (KeyError, ValueError):
+        return None
 
 
 def read_kernel_profile(lib):
@@ -250,14 +275,115 @@ def cpu_baseline(w, target_s=20.0):
     }
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def ceiling_frac(w):
+    """Roofline ceiling of a workload as a fraction of bf16 MFMA peak: its
+    credited flops (12 d H P) over the minimum HBM bytes of forward and
+    backward in bf16 (36 bytes per (token, head, dim) element: forward reads
+    q, k, v, u and writes y, o; LayerNorm backward reads dy, u, o and writes
+    du, dO; attention backward reads q, k, v, dO and writes dq, dk, dv),
+    times 8 TB/s, capped at 1."""
+    ai = 12.0 * w.d * w.H * w.pairs / (36.0 * w.T * w.H * w.d)
+    return min(1.0, ai * PEAK_HBM_GBS * 1e9 / (PEAK_BF16_TFLOPS * 1e12))
+
+
+class AttnRun:
+    """One workload resident on the GPU with its plan; step() enqueues one
+    forward + backward (forward only for forward-only workloads)."""
+
+    def __init__(self, w, stream):
+        from paper_2605_13433_amd import hstu
+        dev = lambda t: None if t is None else t.contiguous().cuda()
+        self.w = w
+        self.stream = stream
+        self.q, self.k, self.v, self.u, self.off = (
+            dev(x) for x in (w.q, w.k, w.v, w.u, w.seq_offsets))
+        self.dy = dev(w.dy)
+        pos, tw, ts = dev(w.pos_w), dev(w.time_w), dev(w.timestamps)
+        self.bwd = w.dy is not None
+        self.plan = hstu.Plan(self.q, self.off, w.N, pos, tw, ts, w.num_buckets,
+                              backward=self.bwd)
+
+    def step(self):
+        self.plan.forward(self.q, self.k, self.v, self.u, self.off, self.stream)
+        if self.bwd:
+            self.plan.backward(self.q, self.k, self.v, self.u, self.off, self.dy, self.stream)
+
+    def time(self, steps, warmup):
+        """(ms per step, wall seconds of the timed region): HIP events on the
+        launch stream around exactly `steps` steps after `warmup` untimed ones."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record(self.stream)
+        for _ in range(steps):
+            self.step()
+        ev1.record(self.stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / steps, time.perf_counter() - t0
+
+    def kernel_times(self, lib, steps):
+        """Per-kernel averages from the library's event profiler."""
+        import torch
+        lib.hstu_profile_enable(1)
+        for _ in range(steps):
+            self.step()
+        torch.cuda.synchronize()
+        lib.hstu_profile_enable(0)
+        return read_kernel_profile(lib)
+
+
+def config_summary(w, ms, kernels):
+    """One entry of the per-workload report."""
+    flops = (12.0 if w.dy is not None else 4.0) * w.d * w.H * w.pairs
+    tf = flops / (ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype_name == "bf16" else PEAK_FP32_TFLOPS
+    out = {
+        "workload": w.name,
+        "dtype": w.dtype_name,
+        "pass": "fwd+bwd" if w.dy is not None else "fwd",
+        "total_tokens": w.T,
+        "causal_pairs_per_head": w.pairs,
+        "max_seq_len": int(w.lengths.max()),
+        "ms_per_step": round(ms, 5),
+        "TFLOP_s": round(tf, 3),
+        "pct_of_peak": round(100.0 * tf / peak, 3),
+        "peak_TFLOP_s": peak,
+        "kernels_us": {n: round(r["avg_us"], 2) for n, r in kernels.items()},
+    }
+    if w.dy is not None and w.dtype_name == "bf16":
+        c = ceiling_frac(w)
+        out["roofline_ceiling_pct"] = round(100.0 * c, 2)
+        out["pct_of_ceiling"] = round(100.0 * tf / PEAK_BF16_TFLOPS / c, 2)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=5)
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload report of the other workloads")
+    ap.add_argument("--config-steps", type=int, default=20,
+                    help="timed steps of each other workload in the per-workload report")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after a 1 GiB cache flush")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -290,50 +416,26 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     lib = hstu.load_library()
+    stream = torch.cuda.current_stream()
 
     w = inputs.workload(args.workload, args.seed)
     if w.dy is None:
         print(f"workload {args.workload} is forward-only; pick a fwd+bwd workload",
               file=sys.stderr)
         sys.exit(2)
-    dev = lambda t: None if t is None else t.contiguous().cuda()
-    q, k, v, u, off = (dev(x) for x in (w.q, w.k, w.v, w.u, w.seq_offsets))
-    dy = dev(w.dy)
-    pos, tw, ts = dev(w.pos_w), dev(w.time_w), dev(w.timestamps)
-    plan = hstu.Plan(q, off, w.N, pos, tw, ts, w.num_buckets, backward=True)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        plan.forward(q, k, v, u, off, stream)
-        plan.backward(q, k, v, u, off, dy, stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    print(f"[bench] workload {args.workload} {w.name}: T={w.T} pairs/head={w.pairs}",
+          file=sys.stderr, flush=True)
+    run = AttnRun(w, stream)
 
     # ---- timed region: exactly K steps
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall_s = time.perf_counter() - t0
-    ms_per_step = ev0.elapsed_time(ev1) / args.steps
-
+    ms_per_step, wall_s = run.time(args.steps, args.warmup)
     flops_step = 12.0 * w.d * w.H * w.pairs
     value = flops_step / (ms_per_step * 1e-3) / 1e12
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step", file=sys.stderr,
+          flush=True)
 
     # ---- per-kernel durations: HIP events around every launch, same stream
-    lib.hstu_profile_enable(1)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    lib.hstu_profile_enable(0)
-    kernels = read_kernel_profile(lib)
+    kernels = run.kernel_times(lib, args.steps)
 
     # ---- cold cache: flush L2 + MALL (1 GiB of writes) before each step
     cold_ms = None
@@ -345,7 +447,7 @@ def main():
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            step()
+            run.step()
             b.record(stream)
             torch.cuda.synchronize()
             times.append(a.elapsed_time(b))
@@ -371,6 +473,8 @@ def main():
     roof["traffic"] = traffic
     roof["algorithmic_bytes"] = nbytes
     roof["algorithmic_flops"] = nflops
+    clock = load_clock(dominant, w.name, sha)
+    roof["clock_mhz"] = clock
 
     for n, r in kernels.items():
         b, f = kernel_work(n, w, elem_bytes)
@@ -379,6 +483,7 @@ def main():
         r["TFLOP_s"] = round(f / s / 1e12, 2) if f else None
         r["avg_us"] = round(r["avg_us"], 2)
 
+    w.dtype_name = "bf16" if w.dtype == torch.bfloat16 else "f32"
     out = {
         "metric": "jagged HSTU attn fwd+bwd valid-token TFLOP/s + % of bf16 MFMA peak, 1 GPU",
         "value": round(value, 3),
@@ -390,7 +495,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
+        "dtype": w.dtype_name,
         "data": "synthetic (seeded long-tailed jagged lengths, N(0,1) q/k/v/u/dy, "
                 "N(0,0.1) bias tables, Poisson-gap timestamps)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "d": w.d, "max_len": w.N,
@@ -401,17 +506,43 @@ def main():
                    "seed": args.workload if args.seed is None else args.seed,
                    "parallelism": "single GPU"},
         "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 3),
+        "roofline_ceiling_pct": round(100.0 * ceiling_frac(w), 2),
         "wall_s_timed_region": round(wall_s, 4),
         "cold_ms_per_step": None if cold_ms is None else round(cold_ms, 5),
         "cold_value": None if cold_ms is None else round(flops_step / (cold_ms * 1e-3) / 1e12, 3),
         "kernels": kernels,
         "roofline": roof,
         "kernel_source_sha": sha,
+        "gpu": torch.cuda.get_device_name(0),
     }
     if "x" in w.extra:
         out["layer"] = layer_bench(lib, w, args.steps, args.warmup, stream)
+    del run
+    torch.cuda.empty_cache()
+
+    # ---- every workload, timed the same way, beside its roofline ceiling
+    if not args.no_configs:
+        configs = {}
+        for idx in sorted(inputs.WORKLOADS):
+            if idx == args.workload and args.seed is None:
+                configs[str(idx)] = config_summary(w, ms_per_step, kernels)
+                continue
+            wc = inputs.workload(idx)
+            wc.dtype_name = "bf16" if wc.dtype == torch.bfloat16 else "f32"
+            rc = AttnRun(wc, stream)
+            ms, _ = rc.time(args.config_steps, min(args.warmup, 5))
+            kt = rc.kernel_times(lib, args.config_steps)
+            configs[str(idx)] = config_summary(wc, ms, kt)
+            print(f"[bench] workload {idx} {wc.name}: {ms:.4f} ms/step", file=sys.stderr,
+                  flush=True)
+            del rc
+            torch.cuda.empty_cache()
+        out["configs"] = configs
+
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w)
+        cb = cpu_baseline(w)
+        cb["cpu_model"] = cpu_model()
+        out["cpu_baseline"] = cb
     print(json.dumps(out))
 
 

@@ -2,7 +2,7 @@
  * hstu_jagged.h -- C ABI of the MI355X (gfx950) jagged HSTU attention library.
  *
  * Operation.  The paper's jagged fusion operator for attention and RAB
- * (Sec. 3.1.1 "Jagged Fusion Operators for Attention and RAB" and the
+ * (Sec. 4.1.1 "Jagged Fusion Operators for Attention and RAB" and the
  * appendix of the same name) fuses attention with a relative attention bias
  * -- relative position bias (rpb) plus relative time bias (rtb) -- over
  * jagged query/key/value inputs, with no padding and no dense<->jagged
@@ -39,9 +39,14 @@
  *
  * seq_offsets contract (int64, device): off[0] = 0, non-decreasing,
  * 0 <= off[b+1] - off[b] <= max_len, off[B] = total_tokens.  It is read on
- * the device only and is not checked; the kernels clamp each length into
- * [0, max_len] and each row index into [0, total_tokens), so a violating
- * offsets array yields unspecified values but never an out-of-bounds access.
+ * the device only; the kernels clamp each length into [0, max_len] and each
+ * row index into [0, total_tokens), so a violating offsets array yields
+ * unspecified values but never an out-of-bounds access.  It is checked only
+ * when the environment variable HSTU_VALIDATE is "1" at the time of a call:
+ * then the call's scheduler kernel records the violations it finds in a
+ * status word of the workspace (read it with hstu_jagged_status) and, on any
+ * violation, the attention kernels of that call skip their work.  Either
+ * way the call never waits for the device.
  * Empty sequences are legal.  B = 0 or total_tokens = 0 is a successful
  * call; it enqueues nothing, except that a backward call with a bias table
  * still writes that table's gradient (all zeros).
@@ -74,9 +79,18 @@ extern "C" {
 
 #define HSTU_LN_EPS 1e-6f
 
+/* Status word of the seq_offsets contract check (hstu_jagged_status): 0 =
+ * checked and held, else a bitwise OR of the violations found, or
+ * HSTU_SEQ_UNCHECKED when the call ran without HSTU_VALIDATE=1. */
+#define HSTU_SEQ_FIRST_NOT_ZERO 0x1   /* off[0] != 0                        */
+#define HSTU_SEQ_DECREASING 0x2       /* off[b+1] < off[b] for some b       */
+#define HSTU_SEQ_TOO_LONG 0x4         /* off[b+1] - off[b] > max_len        */
+#define HSTU_SEQ_LAST_NOT_T 0x8       /* off[B] != total_tokens             */
+#define HSTU_SEQ_UNCHECKED 0x40000000
+
 typedef enum { HSTU_BF16 = 0, HSTU_F32 = 1 } hstu_dtype;
 
-/* Relative attention bias (Sec. 3.1.1: rpb + rtb).  Either table may be
+/* Relative attention bias (Sec. 4.1.1: rpb + rtb).  Either table may be
  * NULL; with both NULL the bias is zero. */
 typedef struct {
     const float *pos_w;          /* [H][2*max_len-1] float32, or NULL        */
@@ -117,14 +131,14 @@ typedef struct {
     size_t workspace_bytes;      /* >= hstu_jagged_attn_workspace_bytes(..,1) */
 } hstu_bwd_io;
 
-/* Forward: o, y, ln_mean, ln_rstd from q, k, v, u (Sec. 3.1.1). */
+/* Forward: o, y, ln_mean, ln_rstd from q, k, v, u (Sec. 4.1.1). */
 int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
                          const void *u, const int64_t *seq_offsets, int32_t B,
                          int32_t max_len, int32_t H, int32_t d,
                          const hstu_rab *rab, hstu_fwd_out *out, void *stream);
 
 /* Backward: dq, dk, dv, du, d_pos_w, d_time_w of sum(y * dy), given the
- * forward's saved o / ln_mean / ln_rstd (Sec. 3.1.1; the table gradients are
+ * forward's saved o / ln_mean / ln_rstd (Sec. 4.1.1; the table gradients are
  * the paper's "RAB backward"). */
 int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
                          const void *u, const int64_t *seq_offsets, int32_t B,
@@ -223,7 +237,7 @@ size_t hstu_layer_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
  * into (sequence, 64-row tile) entries; a query tile costs its tile index
  * + 1 key tiles (causal), a key tile the sequence's tiles minus its index.
  * Both lists are longest first -- the sort-by-cost, assign-greedily
- * balancing of Sec. 3.1.3 applied to the compute units of one GPU -- in one
+ * balancing of Sec. 4.1.3 applied to the compute units of one GPU -- in one
  * of two orders: every entry by cost, or, when the causal tile pairs reach
  * 4 x the longest entry x 4 x (compute units), sequence by sequence
  * (longest sequence first, each sequence's tiles longest first), which
@@ -238,6 +252,15 @@ int hstu_jagged_schedule(const int64_t *seq_offsets, int32_t B,
                          int32_t max_len, int64_t total_tokens,
                          int32_t *n_entries, int32_t *list_q, int32_t *list_k,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* Enqueues on `stream` a copy of the seq_offsets status word (HSTU_SEQ_*)
+ * that the last call which used `workspace` wrote there, into `status`
+ * (one int32, device or host memory; host memory is written when the copy
+ * runs, so the caller synchronises before reading it).  The word is written
+ * by every attention or layer call that enqueues work (calls with
+ * total_tokens = 0 enqueue none, see above); a layer call's workspace
+ * holds it at the same place.  Never waits for the device. */
+int hstu_jagged_status(const void *workspace, int32_t *status, void *stream);
 
 /* Diagnostics: per-kernel timing.  While enabled, every kernel the library
  * launches is bracketed by two HIP events recorded on the stream it is

@@ -7,7 +7,7 @@
  * slow, obviously correct computation.  It shares no code, header, table or
  * helper with the HIP library.
  *
- * What it computes.  The paper (Sec. 3.1.1 "Jagged Fusion Operators for
+ * What it computes.  The paper (Sec. 4.1.1 "Jagged Fusion Operators for
  * Attention and RAB", and its appendix of the same name) fuses attention with
  * a relative attention bias (RAB = relative position bias + relative time
  * bias) over jagged inputs without padding, for HSTU-style models

@@ -7,6 +7,7 @@
 #include <atomic>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -73,6 +74,8 @@ int validate(const void *q, const void *k, const void *v, const void *u,
                   (long long)H * nb);
   }
   p->B = B; p->N = N; p->H = H; p->d = d; p->T = T; p->dtype = dtype;
+  const char *chk = getenv("HSTU_VALIDATE");
+  p->check_offsets = chk && chk[0] == '1';
   p->has_pos = has_pos; p->has_time = has_time; p->nb = nb;
   // sum_b ceil(L_b/64) <= min(B * ceil(N/64), floor((T + 63 B) / 64))
   p->max_entries = std::min<int64_t>((int64_t)B * ceil_div(N, TILE),
@@ -361,6 +364,16 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
     e = launch_attn_bwd_f32(a, ws + L.dO, io->dq, io->dk, io->dv, d_pos, d_time, s);
     if (e != hipSuccess) return hip_fail(e, "attention backward launch");
   }
+  return HSTU_OK;
+}
+
+int hstu_jagged_status(const void *workspace, int32_t *status, void *stream) {
+  g_last_error.clear();
+  if (!workspace || !status) return fail(HSTU_EINVAL, "workspace and status must be non-null");
+  const char *ws = (const char *)workspace;
+  const hipError_t e = hipMemcpyAsync(status, ws + sizeof(int32_t) * CTRL_STATUS,
+                                      sizeof(int32_t), hipMemcpyDefault, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "status copy");
   return HSTU_OK;
 }
 

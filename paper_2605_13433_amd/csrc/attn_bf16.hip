@@ -1,4 +1,4 @@
-// bf16 MFMA kernels of jagged HSTU attention for gfx950 (Sec. 3.1.1: jagged
+// bf16 MFMA kernels of jagged HSTU attention for gfx950 (Sec. 4.1.1: jagged
 // QKV with the relative position and relative time biases fused into the
 // attention kernel, no padding and no dense<->jagged conversion).
 //

@@ -31,6 +31,7 @@ enum CtrlSlot {
   CTRL_POP_DKV = 3,     // pop counter of the dK/dV kernel (and fp32 pass)
   CTRL_POP_BWD = 4,     // pop counter of the combined bf16 backward kernel
   CTRL_N_BWD = 5,       // entries in the combined backward list
+  CTRL_STATUS = 6,      // seq_offsets contract status (HSTU_SEQ_* word)
   CTRL_WORDS = 64
 };
 
@@ -64,6 +65,7 @@ struct Problem {
   bool has_pos, has_time;
   int32_t nb;
   int64_t max_entries;   // upper bound on sum_b ceil(L_b / 64)
+  bool check_offsets;    // HSTU_VALIDATE=1: the scheduler checks the contract
 };
 
 // Workspace carve-up; offsets in bytes from the workspace base, each region

@@ -4,8 +4,9 @@
 // normalise (one launch fewer per backward call).
 //
 // The paper balances jagged work by sorting samples by cost and assigning
-// them greedily (Sec. 3.1.3, "Global Token Reallocation"), and balances
-// work across the compute elements of one device (Sec. 3.1.1, step 3).  On
+// them greedily (Sec. 4.1.3, "Global Token Reallocation"), and balances
+// work across the compute elements of one device (Sec. 4.1.1, "Load
+// balancing across device computing elements").  On
 // one GPU the same idea becomes a longest-first work list consumed by
 // persistent work-groups through an atomic pop counter (every entry expands
 // to H adjacent items, one per head):
@@ -58,6 +59,7 @@ struct SchedSmem {
   int32_t sstart[SCHED_MAX_BINS];     // sequence-major: first entry of bin n's sequences
   int32_t total;
   int32_t seq_major;
+  int32_t status;                     // HSTU_SEQ_* bits found by the contract check
 };
 
 struct SchedArgs {
@@ -71,6 +73,7 @@ struct SchedArgs {
   int32_t H;
   int32_t grid_hint;                  // nominal persistent work-groups
   int32_t fuse_dq0;                   // no dQ entries for first q-tiles
+  int32_t check;                      // check the seq_offsets contract
   float *zero_out;
   int32_t n_zero;
 };
@@ -83,13 +86,25 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     sm.count[c] = 0;
     sm.fill[c] = 0;
   }
-  if (tid == 0) sm.total = 0;
+  if (tid == 0) {
+    sm.total = 0;
+    sm.status = 0;
+  }
   __syncthreads();
 
   // Clamp every sequence into [0, N] rows and into [0, T): a violating
-  // offsets array must never make a kernel read outside its buffers.
+  // offsets array must never make a kernel read outside its buffers.  With
+  // the contract check on, each violation sets its bit of the status word.
   for (int b = tid; b < a.B; b += NT) {
     int64_t s = a.off[b], e = a.off[b + 1];
+    if (a.check) {
+      int bad = 0;
+      if (b == 0 && s != 0) bad |= HSTU_SEQ_FIRST_NOT_ZERO;
+      if (e < s) bad |= HSTU_SEQ_DECREASING;
+      else if (e - s > a.N) bad |= HSTU_SEQ_TOO_LONG;
+      if (b == a.B - 1 && e != a.T) bad |= HSTU_SEQ_LAST_NOT_T;
+      if (bad) atomicOr(&sm.status, bad);
+    }
     s = s < 0 ? 0 : (s > a.T ? a.T : s);
     e = e < s ? s : (e > a.T ? a.T : e);
     int64_t L = e - s;
@@ -127,6 +142,7 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     // ones can, and then only the first `cap` slots are kept -- every slot
     // below the total is filled exactly once, so the kept prefix is dense.
     a.ctrl[CTRL_N_ENTRIES] = sm.total < a.cap ? sm.total : a.cap;
+    a.ctrl[CTRL_STATUS] = a.check ? sm.status : HSTU_SEQ_UNCHECKED;
     a.ctrl[CTRL_POP_FWD] = 0;
     a.ctrl[CTRL_POP_DQ] = 0;
     a.ctrl[CTRL_POP_DKV] = 0;
@@ -135,6 +151,11 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     // first q-tile
     const int32_t n_bwd = 2 * sm.total - (a.fuse_dq0 ? sm.rank0[1] + sm.count[1] : 0);
     a.ctrl[CTRL_N_BWD] = n_bwd < 2 * a.cap ? n_bwd : 2 * a.cap;
+    // a violated contract: the attention kernels find empty lists and skip
+    if (sm.status != 0) {
+      a.ctrl[CTRL_N_ENTRIES] = 0;
+      a.ctrl[CTRL_N_BWD] = 0;
+    }
   }
   __syncthreads();
 
@@ -193,6 +214,7 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.H = p.H;
   a.grid_hint = 4 * L.num_cu;
   a.fuse_dq0 = L.list_b && L.bwd_combined && p.d == 64 ? 1 : 0;
+  a.check = p.check_offsets ? 1 : 0;
   a.zero_out = L.dtime_part ? (float *)(base + L.dtime_part) : nullptr;
   a.n_zero = L.dtime_part ? DTIME_BINS * p.H * p.nb : 0;
   return a;

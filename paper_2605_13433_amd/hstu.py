@@ -23,6 +23,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhstu_jagged.so")
 
 HSTU_BF16, HSTU_F32 = 0, 1
+# seq_offsets status word bits (include/hstu_jagged.h)
+HSTU_SEQ_FIRST_NOT_ZERO = 0x1
+HSTU_SEQ_DECREASING = 0x2
+HSTU_SEQ_TOO_LONG = 0x4
+HSTU_SEQ_LAST_NOT_T = 0x8
+HSTU_SEQ_UNCHECKED = 0x40000000
 ERRORS = {-1: "HSTU_EINVAL", -2: "HSTU_ENOTSUP", -3: "HSTU_EWORKSPACE", -4: "HSTU_EHIP"}
 
 
@@ -105,6 +111,8 @@ def load_library(path: str = LIB_PATH):
     lib.hstu_layer_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i64, i32,
                                                ctypes.c_int, ctypes.POINTER(Rab)]
     lib.hstu_layer_workspace_bytes.restype = ctypes.c_size_t
+    lib.hstu_jagged_status.argtypes = [P, P, P]
+    lib.hstu_jagged_status.restype = ctypes.c_int
     lib.hstu_last_error.argtypes = []
     lib.hstu_last_error.restype = ctypes.c_char_p
     lib.hstu_version.argtypes = []
@@ -208,6 +216,12 @@ def hstu_layer_bwd(x, w1, w2, seq_offsets, B, max_len, H, d, d_model,
         ctypes.byref(io), _stream(stream)))
 
 
+def hstu_jagged_status(workspace, status, stream=None) -> None:
+    """Enqueues the copy of the seq_offsets status word of the last call that
+    used `workspace` into `status` (an int32 tensor of one element)."""
+    _check(load_library().hstu_jagged_status(_ptr(workspace), _ptr(status), _stream(stream)))
+
+
 def max_entries(B: int, max_len: int, total_tokens: int) -> int:
     """Capacity of a work list: min(B*ceil(N/64), (T + 63B)/64)."""
     return min(B * ((max_len + 63) // 64), (total_tokens + 63 * B) // 64)
@@ -289,6 +303,13 @@ class Plan:
                             _ptr(self.dq), _ptr(self.dk), _ptr(self.dv), _ptr(self.du),
                             _ptr(self.d_pos), _ptr(self.d_time), _ptr(self.bwd_ws),
                             self.bwd_ws.numel())
+
+    def status(self, backward=False, stream=None) -> int:
+        """The seq_offsets status word (HSTU_SEQ_* bits) of the last forward
+        (or backward) call; waits for the stream."""
+        st = torch.full((1,), -1, dtype=torch.int32, device=self.fwd_ws.device)
+        hstu_jagged_status(self.bwd_ws if backward else self.fwd_ws, st, stream)
+        return int(st.item())
 
     def forward(self, q, k, v, u, seq_offsets, stream=None) -> FwdResult:
         hstu_jagged_attn_fwd(q, k, v, u, seq_offsets, self.B, self.N, self.H, self.d,

@@ -5,7 +5,7 @@ attention arithmetic, so both the HIP path and the CPU oracle may consume what
 it produces.
 
 The paper measures its jagged fusion operators on KuaiRand-27K / Amazon-all
-training runs (Sec. 3.1.1, Appendix A).  Those datasets are not used here;
+training runs (Sec. 4.1.1, Appendix A).  Those datasets are not used here;
 instead each workload below draws sequence lengths from a long-tailed
 distribution of the same character (most users short, a few very long), with
 head geometry taken from the paper's model settings (8 heads x 128 for the

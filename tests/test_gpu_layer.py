@@ -6,9 +6,8 @@ max|gpu - ref| <= 2e-2 max|ref|: out, h (= x w1), the four silu'd planes
 U, V, Q, K, o, y, dx, dw1, dw2 and both table gradients.  The oracle runs in
 float64 on the bf16 inputs with no intermediate rounding, so the bound also
 covers the bf16 rounding of h, z, y and the GEMM outputs on the GPU side.
-The 32-sequence layer workload runs at full size; its token rows are checked
-on sampled whole sequences, its weight and table gradients (sums over every
-token) on the sampled sub-batch and by additivity over sequences.
+The 32-sequence layer workload runs at full size and is checked on every
+token row and on its full weight and table gradients.
 """
 import numpy as np
 import pytest
@@ -17,7 +16,7 @@ import torch
 from oracle import layer as layer_oracle
 from oracle import oracle
 from paper_2605_13433_amd import hstu, inputs
-from tests.gpu_util import check, rows_of, say, to_dev
+from tests.gpu_util import check, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -93,29 +92,16 @@ def test_layer_split_k_weight_gradients():
     compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
 
 
-def test_layer_workload4_sampled():
+def test_layer_workload4_full():
+    """The 32-sequence layer workload (lengths to 4096) at full size: every
+    token row, both weight gradients and both tables against the oracle."""
     w = inputs.workload(4)
-    say(f"layer workload {w.name}: T={w.T} pairs/head={w.pairs} (full-size GPU run)")
+    say(f"layer workload {w.name}: T={w.T} pairs/head={w.pairs} max L={int(w.lengths.max())}")
     got = run_layer(w)
-    L = w.lengths
-    order = np.argsort(L)
-    rng = np.random.default_rng(44)
-    fits = [int(b) for b in order if L[b] * (L[b] + 1) // 2 <= 1_500_000]
-    chosen = {int(order[0]), fits[-1]} | set(int(b) for b in rng.choice(fits, 3, replace=False))
-    seqs = sorted(chosen)
-    sub = inputs.subset(w, seqs)
-    say(f"  sampled sequences {seqs} lengths {L[seqs].tolist()}")
-    ref = layer_oracle.layer_bwd_workload(sub)
-    compare_layer(w, got, ref, rows=rows_of(w, seqs), sums=False)
-    say("  weight and table gradients on the sampled sub-batch:")
-    got_sub = run_layer(sub)
-    compare_layer(sub, got_sub, ref)
-    rest = [b for b in range(w.B) if b not in chosen]
-    got_rest = run_layer(inputs.subset(w, rest))
-    # additivity over sequences; the weight gradients are bf16 outputs, so
-    # each of the three carries its own rounding
-    for n, tol in (("dw1", 1e-2), ("dw2", 1e-2), ("d_pos", 1e-3), ("d_time", 1e-3)):
-        check(n + "+", got_sub[n] + got_rest[n], got[n], tol)
+    for n, a in got.items():
+        if a is not None:
+            assert np.all(np.isfinite(a)), f"non-finite values in {n}"
+    compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
 
 
 def test_layer_routes_planes_into_attention_bitwise():

@@ -6,9 +6,9 @@ checked as well as y: LayerNorm is scale-invariant, so a wrong global scale
 of o would hide in y).  Small cases span several 64-row tiles, ragged tails,
 empty and single-token sequences and L = max_len; the five workloads run at
 full size in the launch configuration the benchmark times, with the oracle
-on every row for the small ones and on sampled whole sequences for the
-large ones.  Sequence handling (offsets, masks, isolation) is checked
-bit-exactly.
+on every row and both tables for workloads 1-4, and on sampled whole
+sequences (always the longest ones) for the 1024-sequence Zipf batch.
+Sequence handling (offsets, masks, isolation) is checked bit-exactly.
 """
 import numpy as np
 import pytest
@@ -137,28 +137,68 @@ def test_workload2_full():
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
-def _sampled(index, picks, max_pairs):
-    """Full-size GPU run; oracle on sampled whole sequences.  Table
-    gradients sum over every sequence, so they are checked on the sampled
-    sub-batch run by itself, and the full batch's tables must equal the sum
-    of the sample's and the complement's (additivity over sequences)."""
-    w = inputs.workload(index)
-    say(f"workload {index} {w.name}: T={w.T} pairs/head={w.pairs} (full-size GPU run)")
+def assert_finite(got):
+    """Every element of every output of a full-size run is finite (the
+    oracle comparisons of sampled runs only see the sampled rows)."""
+    for n, a in got.items():
+        if a is not None:
+            assert np.all(np.isfinite(a)), f"non-finite values in {n}"
+
+
+def test_workload3_full():
+    """Long-tail batch (d=128, lengths to 2048): every row and both
+    full-batch tables against the oracle."""
+    w = inputs.workload(3)
+    say(f"workload 3 {w.name}: T={w.T} pairs/head={w.pairs} max L={int(w.lengths.max())}")
     got = run_gpu(w)
+    assert_finite(got)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def test_workload4_attention_full():
+    """Layer batch's attention (d=128, lengths to 4096): every row and both
+    full-batch tables against the oracle."""
+    w = inputs.workload(4)
+    say(f"workload 4 {w.name}: T={w.T} pairs/head={w.pairs} max L={int(w.lengths.max())}")
+    got = run_gpu(w)
+    assert_finite(got)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def test_workload5_sampled():
+    """Zipf batch (1024 sequences to 8192 tokens) at full size.  The oracle
+    runs on whole sequences: the four longest (they hold most of the causal
+    pairs), two more above 2M pairs, the two shortest and random picks.
+    Table gradients sum over every sequence; the oracle checks them three
+    ways: on the sampled sub-batch run by itself; on the full batch at every
+    diagonal m >= L of the fifth-longest sequence (only the four sampled
+    longest sequences reach those diagonals, so there the full batch's
+    d_pos equals the sub-batch oracle's); and the full batch's table must be
+    the sum of the sample's and the complement's (additivity)."""
+    w = inputs.workload(5)
+    say(f"workload 5 {w.name}: T={w.T} pairs/head={w.pairs} (full-size GPU run)")
+    got = run_gpu(w)
+    assert_finite(got)
     L = w.lengths
-    order = np.argsort(L)
-    rng = np.random.default_rng(index)
-    chosen = set(int(b) for b in order[:2])                     # shortest
-    fits = [int(b) for b in order if L[b] * (L[b] + 1) // 2 <= max_pairs]
-    chosen.add(fits[-1])                                        # longest that fits
-    chosen |= set(int(b) for b in rng.choice(fits, size=picks, replace=False))
+    order = np.argsort(L, kind="stable")
+    rng = np.random.default_rng(5)
+    chosen = set(int(b) for b in order[:2]) | set(int(b) for b in order[-4:])
+    big = [int(b) for b in order[:-4] if L[b] * (L[b] + 1) // 2 > 2_000_000]
+    chosen |= set(int(b) for b in rng.choice(big, size=2, replace=False))
+    chosen |= set(int(b) for b in rng.choice(order[:-4], size=6, replace=False))
     seqs = sorted(chosen)
     sub = inputs.subset(w, seqs)
-    say(f"  sampled sequences {seqs} lengths {L[seqs].tolist()}")
+    say(f"  sampled sequences {seqs} lengths {L[seqs].tolist()} "
+        f"({100.0 * sub.pairs / w.pairs:.1f}% of the causal pairs)")
     ref_f = oracle.fwd_workload(sub)
     ref_b = oracle.bwd_workload(sub)
     rows = rows_of(w, seqs)
     compare(w, got, ref_f, ref_b, rows=rows, tables=False)
+    m0 = int(L[order[-5]])                         # fifth-longest length
+    hi = w.N - 1 - m0 + 1                          # index j - i + N - 1 <= N - 1 - m0
+    say(f"  full-batch d_pos at diagonals m >= {m0} (only sampled sequences reach them):")
+    check("d_pos[m>=m0]", got["d_pos"][:, :hi], ref_b["d_pos"][:, :hi], TOL[w.dtype])
+    assert np.all(got["d_pos"][:, w.N:] == 0)      # j > i: no causal pair
     say("  tables on the sampled sub-batch:")
     got_sub = run_gpu(sub)
     compare(sub, got_sub, ref_f, ref_b)
@@ -169,16 +209,31 @@ def _sampled(index, picks, max_pairs):
             check(n + "+", got_sub[n] + got_rest[n], got[n], 1e-3)
 
 
-def test_workload3_sampled():
-    _sampled(3, picks=5, max_pairs=1_200_000)
+def test_long_sequence_d128():
+    """One 4096-token sequence at d=128 with both biases (64 tiles; the
+    dK/dV and dQ items of its first tiles stream 64 tiles each)."""
+    lengths = [4096, 1, 700]
+    say(f"long sequence d=128: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=2, d=128, N=4096, seed=410)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
-def test_workload4_attention_sampled():
-    _sampled(4, picks=3, max_pairs=1_500_000)
-
-
-def test_workload5_sampled():
-    _sampled(5, picks=8, max_pairs=2_000_000)
+@pytest.mark.parametrize("nb", [32, 1])
+@pytest.mark.parametrize("d,dtype", [(64, torch.bfloat16), (128, torch.bfloat16),
+                                     (64, torch.float32)])
+def test_num_buckets(nb, d, dtype):
+    """Bucket counts other than 128: with 32 buckets (HSTU's count) the
+    seeded gaps reach buckets past 31, which clamp to the last one; with one
+    bucket every pair reads bucket 0.  Far timestamps in two sequences drive
+    the exact path's clamp as well."""
+    lengths = [200, 130, 65, 150, 64, 1, 250, 190]
+    say(f"num_buckets={nb} d={d} {dtype}: lengths={lengths}")
+    w = inputs.make_workload(lengths, H=2, d=d, N=256, dtype=dtype, num_buckets=nb,
+                             seed=500 + nb + d)
+    w.timestamps = far_timestamps(lengths, seed=501)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
 # ---------------------------------------------------- bit-exact jagged handling
