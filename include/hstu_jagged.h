@@ -137,6 +137,27 @@ int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
                          int32_t max_len, int32_t H, int32_t d,
                          const hstu_rab *rab, hstu_fwd_out *out, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * forward above with the same arguments, kernels and results, except that
+ * out->workspace and out->workspace_bytes are ignored.  Its workspace is a
+ * fixed array of HSTU_NOALLOC_SCRATCH_BYTES that the library holds on every
+ * GPU it runs on until the process ends; a problem whose forward workspace
+ * (hstu_jagged_attn_workspace_bytes(.., for_bwd = 0, ..)) is larger is
+ * rejected with HSTU_EWORKSPACE (with 4 MiB: up to about 170 000 work-list
+ * entries of 64 tokens, e.g. 10 M tokens of 1024 sequences).  The call
+ * itself allocates nothing, records no profiler events, and never waits
+ * for the device.  All calls on one GPU share its array: calls that overlap
+ * on one GPU (other streams or threads) race and give unspecified results;
+ * serialise them.  The seq_offsets status word of such a call lives in that
+ * array and is not exposed. */
+#define HSTU_NOALLOC_SCRATCH_BYTES (4u << 20)
+int hstu_jagged_attn_fwd_noalloc(const void *q, const void *k, const void *v,
+                                 const void *u, const int64_t *seq_offsets,
+                                 int32_t B, int32_t max_len, int32_t H, int32_t d,
+                                 const hstu_rab *rab, hstu_fwd_out *out,
+                                 void *stream);
+
 /* Backward: dq, dk, dv, du, d_pos_w, d_time_w of sum(y * dy), given the
  * forward's saved o / ln_mean / ln_rstd (Sec. 4.1.1; the table gradients are
  * the paper's "RAB backward"). */

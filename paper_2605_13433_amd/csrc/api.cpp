@@ -203,6 +203,63 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   return L;
 }
 
+
+int attn_fwd_call(const void *q, const void *k, const void *v, const void *u,
+                  const int64_t *seq_offsets, int32_t B, int32_t max_len, int32_t H,
+                  int32_t d, const hstu_rab *rab, hstu_fwd_out *out, void *stream,
+                  const FixedScratch *fixed) {
+  clear_last_error();
+  if (!out) return fail(HSTU_EINVAL, "out is NULL");
+  Problem p;
+  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, out->dtype,
+                    out->total_tokens, &p);
+  if (rc != HSTU_OK) return rc;
+  if (p.T > 0 && (!out->y || !out->o || !out->ln_mean || !out->ln_rstd))
+    return fail(HSTU_EINVAL, "out->y, o, ln_mean and ln_rstd must be non-null");
+  if (p.T == 0) return HSTU_OK;
+  int dev = 0;
+  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
+  Layout L = make_layout(p, false, dev);
+  void *ws = out->workspace;
+  if (fixed) {
+    if (L.total > fixed->bytes)
+      return fail(HSTU_EWORKSPACE,
+                  "this problem needs %zu bytes of workspace; the no-allocation entry "
+                  "point's fixed scratch holds %zu",
+                  L.total, fixed->bytes);
+    if (!(ws = fixed->addr(dev))) return HSTU_EHIP;   // addr() recorded the error
+  } else if ((rc = check_workspace(L, ws, out->workspace_bytes)) != HSTU_OK) {
+    return rc;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a{q, k, v, u,
+             rab ? rab->pos_w : nullptr,
+             p.has_time ? rab->time_w : nullptr,
+             p.has_time ? rab->timestamps : nullptr,
+             ws, L, p};
+  // the no-allocation path never records profiler events (creating one may
+  // allocate)
+  const bool prof_on = !fixed;
+  hipError_t e;
+  {
+    prof::Scope ps(prof_on ? "schedule" : nullptr, s);
+    e = launch_schedule(seq_offsets, p, ws, L, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "schedule launch");
+  {
+    prof::Scope ps(!prof_on ? nullptr : p.dtype == HSTU_BF16 ? "attn_fwd" : "attn_fwd_f32", s);
+    e = p.dtype == HSTU_BF16 ? launch_attn_fwd_bf16(a, out->o, s)
+                             : launch_attn_fwd_f32(a, out->o, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "attention forward launch");
+  {
+    prof::Scope ps(prof_on ? "ln_fwd" : nullptr, s);
+    e = launch_ln_fwd(p, out->o, u, out->y, out->ln_mean, out->ln_rstd, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "layernorm forward launch");
+  return HSTU_OK;
+}
+
 }  // namespace hstu
 
 using namespace hstu;
@@ -266,44 +323,7 @@ int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
                          const void *u, const int64_t *seq_offsets, int32_t B,
                          int32_t max_len, int32_t H, int32_t d,
                          const hstu_rab *rab, hstu_fwd_out *out, void *stream) {
-  g_last_error.clear();
-  if (!out) return fail(HSTU_EINVAL, "out is NULL");
-  Problem p;
-  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, out->dtype,
-                    out->total_tokens, &p);
-  if (rc != HSTU_OK) return rc;
-  if (p.T > 0 && (!out->y || !out->o || !out->ln_mean || !out->ln_rstd))
-    return fail(HSTU_EINVAL, "out->y, o, ln_mean and ln_rstd must be non-null");
-  if (p.T == 0) return HSTU_OK;
-  int dev = 0;
-  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
-  Layout L = make_layout(p, false, dev);
-  if ((rc = check_workspace(L, out->workspace, out->workspace_bytes)) != HSTU_OK)
-    return rc;
-  hipStream_t s = (hipStream_t)stream;
-  AttnArgs a{q, k, v, u,
-             rab ? rab->pos_w : nullptr,
-             p.has_time ? rab->time_w : nullptr,
-             p.has_time ? rab->timestamps : nullptr,
-             out->workspace, L, p};
-  hipError_t e;
-  {
-    prof::Scope ps("schedule", s);
-    e = launch_schedule(seq_offsets, p, out->workspace, L, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "schedule launch");
-  {
-    prof::Scope ps(p.dtype == HSTU_BF16 ? "attn_fwd" : "attn_fwd_f32", s);
-    e = p.dtype == HSTU_BF16 ? launch_attn_fwd_bf16(a, out->o, s)
-                             : launch_attn_fwd_f32(a, out->o, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "attention forward launch");
-  {
-    prof::Scope ps("ln_fwd", s);
-    e = launch_ln_fwd(p, out->o, u, out->y, out->ln_mean, out->ln_rstd, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "layernorm forward launch");
-  return HSTU_OK;
+  return attn_fwd_call(q, k, v, u, seq_offsets, B, max_len, H, d, rab, out, stream, nullptr);
 }
 
 int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,

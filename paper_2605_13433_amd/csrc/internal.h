@@ -115,6 +115,21 @@ const DeviceInfo &device_info(int dev);
 
 Layout make_layout(const Problem &p, bool for_bwd, int dev);
 
+// A fixed device buffer that stands in for the caller's workspace: addr(dev)
+// returns its address on device `dev` (or nullptr after recording the
+// error), `bytes` its size.
+struct FixedScratch {
+  void *(*addr)(int dev);
+  size_t bytes;
+};
+
+// The attention forward (schedule, attention, LayerNorm x U) on the
+// caller's workspace (out->workspace), or, with `fixed`, on that buffer.
+int attn_fwd_call(const void *q, const void *k, const void *v, const void *u,
+                  const int64_t *seq_offsets, int32_t B, int32_t max_len, int32_t H,
+                  int32_t d, const hstu_rab *rab, hstu_fwd_out *out, void *stream,
+                  const FixedScratch *fixed);
+
 
 // ---- launchers (each returns hipSuccess or the launch error) ----
 // Builds the work lists (and zeroes the d_time bins when the layout has

@@ -94,6 +94,9 @@ def load_library(path: str = LIB_PATH):
     lib.hstu_jagged_attn_fwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32,
                                          ctypes.POINTER(Rab), ctypes.POINTER(FwdOut), P]
     lib.hstu_jagged_attn_fwd.restype = ctypes.c_int
+    lib.hstu_jagged_attn_fwd_noalloc.argtypes = [P, P, P, P, P, i32, i32, i32, i32,
+                                                 ctypes.POINTER(Rab), ctypes.POINTER(FwdOut), P]
+    lib.hstu_jagged_attn_fwd_noalloc.restype = ctypes.c_int
     lib.hstu_jagged_attn_bwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32,
                                          ctypes.POINTER(Rab), ctypes.POINTER(BwdIO), P]
     lib.hstu_jagged_attn_bwd.restype = ctypes.c_int
@@ -170,6 +173,16 @@ def hstu_jagged_attn_workspace_bytes(B, max_len, H, d, total_tokens, for_bwd,
 def hstu_jagged_attn_fwd(q, k, v, u, seq_offsets, B, max_len, H, d,
                          rab: Optional[Rab], out: FwdOut, stream=None) -> None:
     _check(load_library().hstu_jagged_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(seq_offsets), int(B),
+        int(max_len), int(H), int(d), ctypes.byref(rab) if rab is not None else None,
+        ctypes.byref(out), _stream(stream)))
+
+
+def hstu_jagged_attn_fwd_noalloc(q, k, v, u, seq_offsets, B, max_len, H, d,
+                                 rab: Optional[Rab], out: FwdOut, stream=None) -> None:
+    """As hstu_jagged_attn_fwd on the library's fixed per-GPU scratch
+    (out.workspace is ignored)."""
+    _check(load_library().hstu_jagged_attn_fwd_noalloc(
         _ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(seq_offsets), int(B),
         int(max_len), int(H), int(d), ctypes.byref(rab) if rab is not None else None,
         ctypes.byref(out), _stream(stream)))
