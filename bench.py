@@ -112,7 +112,7 @@ def kernel_work(name, w, elem_bytes):
 def load_traffic(kernel: str, workload: str, sha: str):
     """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
     was taken on the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.txt")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.txt")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -372,6 +372,175 @@ def config_summary(w, ms, kernels):
     return out
 
 
+# ------------------------------------------------------------ counter summaries
+# rocprofv3 passes over one bench.py command (see counters_commands()): a
+# kernel trace for durations, two passes of SQ_ / GRBM_ counters, FETCH_SIZE
+# and WRITE_SIZE; and the same two HBM counters over a 256 MiB device copy
+# (bench.py --copy-probe-mib 256) to calibrate them.
+SQ_PASS_A = ["SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU",
+             "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_ANY",
+             "SQ_ACTIVE_INST_ANY", "SQ_INSTS_VALU", "GRBM_GUI_ACTIVE"]
+SQ_PASS_B = ["SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT",
+             "SQ_INSTS_VALU_TRANS_F32", "SQ_WAIT_INST_LDS", "SQ_THREAD_CYCLES_VALU",
+             "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_LDS_IDX_ACTIVE"]
+SHORT_KERNEL = {"attn_fwd_kernel": "attn_fwd", "attn_bwd_kernel": "attn_bwd",
+                "attn_bwd_dkv_kernel": "attn_bwd_dkv", "attn_bwd_dq_kernel": "attn_bwd_dq",
+                "ln_fwd_kernel": "ln_fwd", "ln_bwd_kernel": "ln_bwd",
+                "schedule_kernel": "schedule", "finalize_tables_kernel": "finalize_tables"}
+
+
+def counters_commands(workload: int):
+    run = (f"python3 bench.py --workload {workload} --steps 5 --warmup 2 --no-cpu-baseline "
+           f"--cold-steps 0 --no-configs")
+    return {
+        "trace": f"rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o trace -- {run}",
+        "sq_a": f"rocprofv3 --pmc {' '.join(SQ_PASS_A)} --output-format csv -d <dir> -o sqa -- {run}",
+        "sq_b": f"rocprofv3 --pmc {' '.join(SQ_PASS_B)} --output-format csv -d <dir> -o sqb -- {run}",
+        "fetch": f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -o fetch -- {run}",
+        "write": f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir> -o write -- {run}",
+        "calibration": ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv "
+                        "-d <dir> -o cal_fetch (cal_write) -- python3 bench.py --copy-probe-mib 256"),
+    }
+
+
+def _kernel_key(name: str):
+    import re
+    m = re.search(r"(\w+_kernel|__amd_rocclr_copyBuffer)(<[^>]*>)?", name)
+    if not m:
+        return None
+    base = m.group(1)
+    return base, (m.group(2) or "")
+
+
+def _read_counters(path):
+    """{(kernel, template): {counter: [per-dispatch values]}} from a rocprofv3
+    counter_collection.csv (one row per dispatch and counter)."""
+    import csv
+    import collections
+    out = collections.defaultdict(lambda: collections.defaultdict(list))
+    with open(path) as fh:
+        for row in csv.DictReader(fh):
+            key = _kernel_key(row["Kernel_Name"])
+            if key:
+                out[key][row["Counter_Name"]].append(float(row["Counter_Value"]))
+    return out
+
+
+def summarize_counters(d, workload, num_cu=256):
+    """Per-kernel counter summaries of one workload from the rocprofv3 output
+    directory `d`; returns {short kernel name: text}."""
+    import csv
+    import glob
+    w_name = inputs_name(workload)
+    # the kernel-source hash of the code that ran: from the bench JSON line
+    # the profiled runs printed
+    sha = None
+    for f in sorted(glob.glob(os.path.join(d, "*.log"))):
+        with open(f) as fh:
+            for line in fh:
+                if line.startswith("{") and "kernel_source_sha" in line:
+                    sha = json.loads(line)["kernel_source_sha"]
+    if sha is None:
+        raise SystemExit(f"no bench.py JSON line with kernel_source_sha under {d}")
+    durs = {}
+    for f in glob.glob(os.path.join(d, "*trace_kernel_stats.csv")):
+        with open(f) as fh:
+            for row in csv.DictReader(fh):
+                key = _kernel_key(row["Name"])
+                if key:
+                    durs[key] = (float(row["AverageNs"]) / 1e3, int(row["Calls"]))
+    cnt = {}
+    for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+        for key, c in _read_counters(f).items():
+            cnt.setdefault(key, {}).update(c)
+    cal = {}
+    for tag, name in (("cal_fetch", "FETCH_SIZE"), ("cal_write", "WRITE_SIZE")):
+        for f in glob.glob(os.path.join(d, f"{tag}*counter_collection.csv")):
+            for key, c in _read_counters(f).items():
+                if key[0] == "__amd_rocclr_copyBuffer" and name in c:
+                    cal[name] = max(c[name])
+    copy_kib = 256 * 1024.0
+    fscale = copy_kib / cal["FETCH_SIZE"] if cal.get("FETCH_SIZE") else None
+    wscale = copy_kib / cal["WRITE_SIZE"] if cal.get("WRITE_SIZE") else None
+    # GPU geometry from the profiler's agent table: GRBM_GUI_ACTIVE is summed
+    # over the XCDs (accelerator dies), each with its own clock counter
+    num_xcc, num_cu = 8, num_cu
+    for f in glob.glob(os.path.join(d, "*agent_info.csv")):
+        with open(f) as fh:
+            for row in csv.DictReader(fh):
+                if row.get("Agent_Type") == "GPU" or row.get("Num_Xcc", "0") not in ("0", ""):
+                    if int(row.get("Cu_Count") or 0) > 0:
+                        num_xcc = int(row["Num_Xcc"])
+                        num_cu = int(row["Cu_Count"])
+    cmds = counters_commands(workload)
+    out = {}
+    for key, c in cnt.items():
+        short = SHORT_KERNEL.get(key[0])
+        if not short or key not in durs:
+            continue
+        avg = {n: sum(v) / len(v) for n, v in c.items()}
+        us, calls = durs[key]
+        lines = [f"# rocprofv3 counters: {key[0]}{key[1]}, workload {w_name}",
+                 "# commands (each a run of its own; <dir> = the output directory):"]
+        lines += [f"#   {k}: {v}" for k, v in cmds.items()]
+        lines += ["# values: mean over the kernel's dispatches in the run.  GRBM_GUI_ACTIVE"
+                  f" sums the {num_xcc} XCDs' busy cycles: clock = GRBM_GUI_ACTIVE / {num_xcc}"
+                  " / duration;",
+                  f"# SIMD-cycles = GRBM_GUI_ACTIVE / {num_xcc} x {num_cu} CUs x 4 SIMDs;"
+                  " SQ_VALU_MFMA_BUSY_CYCLES counts SIMD-cycles (32 per 32x32x16 MFMA);",
+                  "# SQ_ACTIVE_INST_VALU and SQ_ACTIVE_INST_LDS count quad-cycles (x4);"
+                  " SQ_LDS_IDX_ACTIVE counts CU-cycles.",
+                  f"source_sha: {sha}",
+                  f"dispatches_traced: {calls}",
+                  f"trace_avg_us: {us:.2f}"]
+        for n in SQ_PASS_A + SQ_PASS_B + ["FETCH_SIZE", "WRITE_SIZE"]:
+            if n in avg:
+                lines.append(f"{n}: {avg[n]:.1f}")
+        g = avg.get("GRBM_GUI_ACTIVE")
+        if g:
+            cyc = g / num_xcc                     # busy cycles of one XCD
+            simd = cyc * num_cu * 4
+            lines.append(f"clock_mhz: {cyc / us:.0f}")
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
+                lines.append(f"mfma_busy_frac: {avg['SQ_VALU_MFMA_BUSY_CYCLES'] / simd:.4f}")
+            if "SQ_INSTS_MFMA" in avg:
+                # v_mfma_f32_32x32x16_bf16: 8 passes of 4 cycles on one SIMD
+                lines.append(f"mfma_insts_x32_frac: {avg['SQ_INSTS_MFMA'] * 32 / simd:.4f}")
+            if "SQ_ACTIVE_INST_VALU" in avg:
+                lines.append(f"valu_busy_frac: {4 * avg['SQ_ACTIVE_INST_VALU'] / simd:.4f}")
+            if "SQ_ACTIVE_INST_LDS" in avg:
+                lines.append(f"lds_inst_busy_frac: {4 * avg['SQ_ACTIVE_INST_LDS'] / simd:.4f}")
+            if "SQ_LDS_IDX_ACTIVE" in avg:
+                lines.append(f"lds_idx_active_frac: "
+                             f"{avg['SQ_LDS_IDX_ACTIVE'] / (cyc * num_cu):.4f}")
+        if "SQ_INSTS_MFMA" in avg and avg["SQ_INSTS_MFMA"] > 0:
+            m = avg["SQ_INSTS_MFMA"]
+            for n, lab in (("SQ_INSTS_VALU", "valu"), ("SQ_INSTS_VALU_TRANS_F32", "trans"),
+                           ("SQ_INSTS_LDS", "lds")):
+                if n in avg:
+                    lines.append(f"{lab}_insts_per_mfma: {avg[n] / m:.3f}")
+        if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_LDS_IDX_ACTIVE"):
+            lines.append(f"lds_bank_conflict_per_idx_active: "
+                         f"{avg['SQ_LDS_BANK_CONFLICT'] / avg['SQ_LDS_IDX_ACTIVE']:.4f}")
+        if "FETCH_SIZE" in avg and fscale:
+            lines += [f"fetch_kib_per_dispatch: {avg['FETCH_SIZE']:.1f}",
+                      f"fetch_scale: {fscale:.4f}"]
+        if "WRITE_SIZE" in avg and wscale:
+            lines += [f"write_kib_per_dispatch: {avg['WRITE_SIZE']:.1f}",
+                      f"write_scale: {wscale:.4f}"]
+        if "FETCH_SIZE" in avg and "WRITE_SIZE" in avg and fscale and wscale:
+            hbm = (avg["FETCH_SIZE"] * fscale + avg["WRITE_SIZE"] * wscale) * 1024.0
+            lines += [f"hbm_bytes_per_dispatch: {hbm:.0f}",
+                      f"hbm_GB_s: {hbm / (us * 1e-6) / 1e9:.1f}"]
+        out[short] = "\n".join(lines) + "\n"
+    return out
+
+
+def inputs_name(workload: int) -> str:
+    from paper_2605_13433_amd import inputs
+    return inputs.WORKLOADS[workload]["name"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -388,7 +557,19 @@ def main():
                     help="extra steps, each after a 1 GiB cache flush")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device copies of this many MiB (counter calibration)")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="only write profiles/<kernel>_<workload>_counters.txt from the "
+                         "rocprofv3 output in DIR (see counters_commands)")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        for short, text in summarize_counters(args.summarize_counters, args.workload).items():
+            path = os.path.join(ROOT, "profiles",
+                                f"{short}_{inputs_name(args.workload)}_counters.txt")
+            with open(path, "w") as fh:
+                fh.write(text)
+            print(path)
+        return
 
     if args.copy_probe_mib:
         import torch
