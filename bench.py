@@ -225,6 +225,67 @@ def layer_bench(lib, w, steps, warmup, stream):
     }
 
 
+def embedding_bench(stream, steps, warmup, dtype_name="f32"):
+    """The jagged multi-table embedding lookup on the sequence-feature batch
+    (8 tables of 128 .. 4 M rows, 32 sequences of 1 .. 4160 tokens, D = 128,
+    token-major output): forward and backward times with HIP events on the
+    launch stream, and the forward's HBM roofline (algorithmic bytes: the id,
+    the table row read and the output row written per id)."""
+    import torch
+    from paper_2605_13433_amd import emb_inputs
+    from paper_2605_13433_amd import embedding as emb
+    dtype = torch.float32 if dtype_name == "f32" else torch.bfloat16
+    b = emb_inputs.sequence_batch(dtype=dtype)
+    W = b.weights.cuda()
+    ids = b.ids.cuda()
+    ro, io = b.row_offsets.cuda(), b.id_offsets.cuda()
+    dout = emb_inputs.token_layout(b.dout, b.F).cuda()
+    p = emb.plan(W, ro, io, b.total_rows, b.n, "token")
+    out = torch.empty(p.out_shape, dtype=W.dtype, device="cuda")
+    grad = torch.zeros(b.total_rows, b.D, dtype=torch.float32, device="cuda")
+    uniq = torch.empty(b.n, dtype=torch.int64, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn()
+        z.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / steps * 1e3
+
+    fwd_us = timed(lambda: emb.lookup(p, W, ids, out, stream))
+    pf = emb.plan(W, ro, io, b.total_rows, b.n, "flat", with_bwd=False)
+    out_flat = torch.empty(pf.out_shape, dtype=W.dtype, device="cuda")
+    fwd_flat_us = timed(lambda: emb.lookup(pf, W, ids, out_flat, stream))
+    del out_flat
+    bwd_us = timed(lambda: emb.lookup_backward(p, ids, dout, grad, uniq, cnt, stream))
+    U = int(cnt.item())
+    es = W.element_size()
+    fwd_bytes = b.n * (8 + 2 * b.D * es)
+    bwd_bytes = b.n * (8 + b.D * es) + U * (b.D * 4 + 8)
+    fwd_gbs = fwd_bytes / (fwd_us * 1e-6) / 1e9
+    padded = b.F * len(b.lengths) * emb_inputs.EMB_MAX_LEN
+    return {
+        "workload": b.name,
+        "tables": b.F, "rows": [int(r) for r in b.rows], "D": b.D, "dtype": dtype_name,
+        "num_ids": b.n, "padded_ids": padded, "distinct_rows": U,
+        "fwd_us": round(fwd_us, 2), "bwd_us": round(bwd_us, 2),
+        "fwd_flat_layout_us": round(fwd_flat_us, 2),
+        "fwd_GB_s": round(fwd_gbs, 1),
+        "bwd_GB_s": round(bwd_bytes / (bwd_us * 1e-6) / 1e9, 1),
+        "roofline": {"bound": "hbm", "kernel": "emb_fwd", "achieved": round(fwd_gbs, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(fwd_gbs / PEAK_HBM_GBS, 4),
+                     "algorithmic_bytes": fwd_bytes},
+    }
+
+
 def cpu_baseline(w, target_s=20.0):
     """The oracle, as it stands, on a bounded sample of the same workload:
     whole sequences in a seeded random order until the estimated
@@ -555,6 +616,10 @@ def main():
                     help="timed steps of each other workload in the per-workload report")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after a 1 GiB cache flush")
+    ap.add_argument("--no-embedding", action="store_true",
+                    help="skip the embedding-lookup measurement")
+    ap.add_argument("--embedding-only", action="store_true",
+                    help="only time the embedding lookup (prints its JSON object)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device copies of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
@@ -598,6 +663,11 @@ def main():
     torch.cuda.set_device(0)
     lib = hstu.load_library()
     stream = torch.cuda.current_stream()
+
+    if args.embedding_only:
+        for dt in ("f32", "bf16"):
+            print(json.dumps(embedding_bench(stream, args.steps, args.warmup, dt)), flush=True)
+        return
 
     w = inputs.workload(args.workload, args.seed)
     if w.dy is None:
@@ -719,6 +789,10 @@ def main():
             del rc
             torch.cuda.empty_cache()
         out["configs"] = configs
+
+    if not args.no_embedding:
+        out["embedding"] = embedding_bench(stream, args.config_steps, min(args.warmup, 5))
+        torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         cb = cpu_baseline(w)

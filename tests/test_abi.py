@@ -10,14 +10,15 @@ import pytest
 from paper_2605_13433_amd import hstu
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "hstu_jagged.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 
 pytestmark = pytest.mark.skipif(not os.path.exists(hstu.LIB_PATH),
                                 reason="libhstu_jagged.so not built")
 
 
 def declared_functions():
-    src = open(HEADER).read()
+    src = "\n".join(open(h).read() for h in HEADERS)
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(hstu_\w+)\s*\(", src, flags=re.M)))
 
@@ -25,7 +26,9 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     names = declared_functions()
     assert {"hstu_jagged_attn_fwd", "hstu_jagged_attn_bwd",
-            "hstu_jagged_attn_workspace_bytes", "hstu_last_error"} <= set(names)
+            "hstu_jagged_attn_workspace_bytes", "hstu_last_error",
+            "hstu_jagged_embedding_fwd", "hstu_jagged_embedding_bwd",
+            "hstu_jagged_embedding_bwd_workspace_bytes"} <= set(names)
     lib = ctypes.CDLL(hstu.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
