@@ -17,11 +17,15 @@
  * specified for this library:
  *
  *   for every sequence b (rows off[b] .. off[b+1]-1), head h, local i, j:
- *     s_ij = <q_i, k_j> + w_pos[h, j - i + N - 1] + w_time[h, bucket(ts_i - ts_j)]
+ *     s_ij = alpha <q_i, k_j> + w_pos[h, j - i + N - 1] + w_time[h, bucket(ts_i - ts_j)]
  *     a_ij = silu(s_ij) / N  if j <= i, else 0          (N = max_len)
  *     o_i  = sum_j a_ij v_j
  *   per token: z = concat_h o[h]; n = (z - mean z) / sqrt(var z + eps)
  *     (biased variance, no affine); y = n * u.
+ *
+ * alpha is an optional scale of the query-key product (1 gives the plain
+ * operator; the paper's RAB variants include such a scale, unstated in
+ * value, so the library reads it as a caller-chosen constant).
  *
  * Everything is double precision; inputs are the exact values of whatever
  * lower precision the caller used.  Loops run in the plainest order
@@ -92,7 +96,7 @@ static int check_args(const int64_t *off, int32_t B, int32_t N, int32_t H,
 static void attention(const double *q, const double *k, const double *v,
                       const int64_t *off, int32_t B, int32_t N, int32_t H,
                       int32_t d, const double *pos_w, const double *time_w,
-                      const int64_t *ts, int32_t nb, double *o)
+                      const int64_t *ts, int32_t nb, double alpha, double *o)
 {
     const int64_t row = (int64_t)H * d;
     const int64_t nbh = (int64_t)B * H;
@@ -111,7 +115,7 @@ static void attention(const double *q, const double *k, const double *v,
                 const double *vj = v + c * row + (int64_t)h * d;
                 double s = 0.0;
                 for (int32_t e = 0; e < d; ++e) s += qi[e] * kj[e];
-                s += rab(pos_w, time_w, ts, nb, N, h, i, j, r, c);
+                s = alpha * s + rab(pos_w, time_w, ts, nb, N, h, i, j, r, c);
                 const double a = silu(s) / (double)N;
                 for (int32_t e = 0; e < d; ++e) oi[e] += a * vj[e];
             }
@@ -148,13 +152,13 @@ int hstu_oracle_fwd(const double *q, const double *k, const double *v,
                     int32_t max_len, int32_t H, int32_t d,
                     const double *pos_w, const double *time_w,
                     const int64_t *timestamps, int32_t num_buckets, double eps,
-                    double *o, double *y, double *ln_mean, double *ln_rstd)
+                    double alpha, double *o, double *y, double *ln_mean, double *ln_rstd)
 {
     if (check_args(seq_offsets, B, max_len, H, d, time_w, timestamps, num_buckets))
         return -1;
     const int64_t T = seq_offsets[B], row = (int64_t)H * d;
     attention(q, k, v, seq_offsets, B, max_len, H, d, pos_w, time_w,
-              timestamps, num_buckets, o);
+              timestamps, num_buckets, alpha, o);
     ln_stats(o, T, row, eps, ln_mean, ln_rstd);
     for (int64_t r = 0; r < T; ++r)
         for (int64_t f = 0; f < row; ++f)
@@ -167,7 +171,7 @@ int hstu_oracle_fwd(const double *q, const double *k, const double *v,
  *   du = n * dy;  g = dy * u;
  *   do = rstd * (g - mean(g) - n * mean(g * n))            (LayerNorm backward)
  *   dA_ij = <do_i, v_j>;  dS_ij = dA_ij * silu'(s_ij) / N   (j <= i)
- *   dv_j += a_ij do_i;  dq_i += dS_ij k_j;  dk_j += dS_ij q_i;
+ *   dv_j += a_ij do_i;  dq_i += alpha dS_ij k_j;  dk_j += alpha dS_ij q_i;
  *   d_pos[h, j-i+N-1] += dS_ij;  d_time[h, bucket] += dS_ij
  * with silu'(x) = sigma(x) (1 + x (1 - sigma(x))).  All gradients are
  * overwritten.  d_pos_w / d_time_w are required iff the matching table is
@@ -178,7 +182,7 @@ int hstu_oracle_bwd(const double *q, const double *k, const double *v,
                     int32_t max_len, int32_t H, int32_t d,
                     const double *pos_w, const double *time_w,
                     const int64_t *timestamps, int32_t num_buckets, double eps,
-                    const double *dy, double *dq, double *dk, double *dv,
+                    double alpha, const double *dy, double *dq, double *dk, double *dv,
                     double *du, double *d_pos_w, double *d_time_w)
 {
     if (check_args(seq_offsets, B, max_len, H, d, time_w, timestamps, num_buckets))
@@ -196,7 +200,7 @@ int hstu_oracle_bwd(const double *q, const double *k, const double *v,
         free(o); free(dO); free(mean); free(rstd);
         return -2;
     }
-    attention(q, k, v, seq_offsets, B, N, H, d, pos_w, time_w, timestamps, nb, o);
+    attention(q, k, v, seq_offsets, B, N, H, d, pos_w, time_w, timestamps, nb, alpha, o);
     ln_stats(o, T, row, eps, mean, rstd);
 
     /* LayerNorm + gate backward, per token. */
@@ -262,15 +266,15 @@ int hstu_oracle_bwd(const double *q, const double *k, const double *v,
                     double *dvj = dv + c * row + (int64_t)h * d;
                     double s = 0.0, dA = 0.0;
                     for (int32_t e = 0; e < d; ++e) s += qi[e] * kj[e];
-                    s += rab(pos_w, time_w, timestamps, nb, N, h, i, j, r, c);
+                    s = alpha * s + rab(pos_w, time_w, timestamps, nb, N, h, i, j, r, c);
                     for (int32_t e = 0; e < d; ++e) dA += doi[e] * vj[e];
                     const double sg = sigmoid(s);
                     const double a = silu(s) / (double)N;
                     const double dS = dA * sg * (1.0 + s * (1.0 - sg)) / (double)N;
                     for (int32_t e = 0; e < d; ++e) {
                         dvj[e] += a * doi[e];
-                        dqi[e] += dS * kj[e];
-                        dkj[e] += dS * qi[e];
+                        dqi[e] += alpha * dS * kj[e];
+                        dkj[e] += alpha * dS * qi[e];
                     }
                     if (pos_w) my_pos[(int64_t)h * (2 * N - 1) + (j - i + N - 1)] += dS;
                     if (time_w)

@@ -44,10 +44,10 @@ def _load():
         lib.hstu_oracle_time_bucket.argtypes = [i64, i32]
         lib.hstu_oracle_time_bucket.restype = ctypes.c_int
         lib.hstu_oracle_fwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32, P, P,
-                                        P, i32, f64, P, P, P, P]
+                                        P, i32, f64, f64, P, P, P, P]
         lib.hstu_oracle_fwd.restype = ctypes.c_int
         lib.hstu_oracle_bwd.argtypes = [P, P, P, P, P, i32, i32, i32, i32, P, P,
-                                        P, i32, f64, P, P, P, P, P, P, P]
+                                        P, i32, f64, f64, P, P, P, P, P, P, P]
         lib.hstu_oracle_bwd.restype = ctypes.c_int
         lib.hstu_oracle_num_threads.argtypes = []
         lib.hstu_oracle_num_threads.restype = ctypes.c_int
@@ -95,7 +95,7 @@ def _common(q, k, v, u, seq_offsets, pos_w, time_w, timestamps):
 
 
 def fwd(q, k, v, u, seq_offsets, max_len, pos_w=None, time_w=None,
-        timestamps=None, num_buckets=128, eps=EPS):
+        timestamps=None, num_buckets=128, eps=EPS, alpha=1.0):
     """Returns dict(o [T,H,d], y [T,H*d], mean [T], rstd [T])."""
     q, k, v, u, off, T, H, d, pos_w, time_w, ts = _common(
         q, k, v, u, seq_offsets, pos_w, time_w, timestamps)
@@ -105,7 +105,7 @@ def fwd(q, k, v, u, seq_offsets, max_len, pos_w=None, time_w=None,
     mean = np.zeros(T); rstd = np.zeros(T)
     rc = _load().hstu_oracle_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(off),
                                  B, int(max_len), H, d, _ptr(pos_w), _ptr(time_w),
-                                 _ptr(ts), int(num_buckets), float(eps),
+                                 _ptr(ts), int(num_buckets), float(eps), float(alpha),
                                  _ptr(o), _ptr(y), _ptr(mean), _ptr(rstd))
     if rc != 0:
         raise ValueError(f"hstu_oracle_fwd rejected its arguments (rc={rc})")
@@ -113,7 +113,7 @@ def fwd(q, k, v, u, seq_offsets, max_len, pos_w=None, time_w=None,
 
 
 def bwd(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=None,
-        timestamps=None, num_buckets=128, eps=EPS):
+        timestamps=None, num_buckets=128, eps=EPS, alpha=1.0):
     """Returns dict(dq, dk, dv [T,H,d], du [T,H*d], d_pos, d_time)."""
     q, k, v, u, off, T, H, d, pos_w, time_w, ts = _common(
         q, k, v, u, seq_offsets, pos_w, time_w, timestamps)
@@ -126,7 +126,7 @@ def bwd(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=None,
     d_time = np.zeros((H, int(num_buckets))) if time_w is not None else None
     rc = _load().hstu_oracle_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(u), _ptr(off),
                                  B, N, H, d, _ptr(pos_w), _ptr(time_w), _ptr(ts),
-                                 int(num_buckets), float(eps), _ptr(dy),
+                                 int(num_buckets), float(eps), float(alpha), _ptr(dy),
                                  _ptr(dq), _ptr(dk), _ptr(dv), _ptr(du),
                                  _ptr(d_pos), _ptr(d_time))
     if rc != 0:
@@ -134,12 +134,12 @@ def bwd(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=None,
     return dict(dq=dq, dk=dk, dv=dv, du=du, d_pos=d_pos, d_time=d_time)
 
 
-def fwd_workload(w, eps=EPS):
+def fwd_workload(w, eps=EPS, alpha=1.0):
     """Oracle forward on a paper_2605_13433_amd.inputs.Workload."""
     return fwd(w.q, w.k, w.v, w.u, w.seq_offsets, w.N, w.pos_w, w.time_w,
-               w.timestamps, w.num_buckets, eps)
+               w.timestamps, w.num_buckets, eps, alpha)
 
 
-def bwd_workload(w, eps=EPS):
+def bwd_workload(w, eps=EPS, alpha=1.0):
     return bwd(w.q, w.k, w.v, w.u, w.seq_offsets, w.N, w.dy, w.pos_w,
-               w.time_w, w.timestamps, w.num_buckets, eps)
+               w.time_w, w.timestamps, w.num_buckets, eps, alpha)

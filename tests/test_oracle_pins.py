@@ -364,3 +364,53 @@ def test_mistakes_are_caught(oracle_lib):
     assert _rel(oracle_lib.fwd_workload(w2)["o"], ref) > 1e-3
     # missing 1/N: scale by N
     assert _rel(f["o"] * N, ref) > 1e-3
+
+
+# ------------------------------------------------ optional scale alpha on QK^T
+def test_alpha_is_a_query_scaling(oracle_lib):
+    """s = alpha <q, k> + rab equals the plain operator on queries alpha*q:
+    forward outputs agree, dq(alpha, q) = alpha dq(1, alpha q), every other
+    gradient agrees (a scale left out of the forward, dq or dk fails)."""
+    w = inputs.make_workload([7, 1, 13, 0, 9], H=2, d=8, N=16, dtype=torch.float64, seed=21)
+    alpha = 0.37
+    f = oracle_lib.fwd_workload(w, alpha=alpha)
+    g = oracle_lib.bwd_workload(w, alpha=alpha)
+    qa = w.q.double() * alpha
+    f1 = oracle_lib.fwd(qa, w.k, w.v, w.u, w.seq_offsets, w.N, w.pos_w, w.time_w,
+                        w.timestamps, w.num_buckets)
+    g1 = oracle_lib.bwd(qa, w.k, w.v, w.u, w.seq_offsets, w.N, w.dy, w.pos_w, w.time_w,
+                        w.timestamps, w.num_buckets)
+    for n in ("o", "y"):
+        assert _rel(f[n], f1[n]) < 1e-13, n
+    assert _rel(g["dq"], alpha * g1["dq"]) < 1e-12
+    for n in ("dk", "dv", "du", "d_pos", "d_time"):
+        assert _rel(g[n], g1[n]) < 1e-12, n
+    # and alpha = 1 is the plain operator
+    f0 = oracle_lib.fwd_workload(w)
+    assert np.array_equal(f0["o"], oracle_lib.fwd_workload(w, alpha=1.0)["o"])
+
+
+def test_alpha_finite_differences(oracle_lib):
+    N, H, d = 8, 2, 4
+    w = inputs.make_workload([5, 6], H=H, d=d, N=N, dtype=torch.float64, seed=22)
+    alpha = -1.7
+    g = oracle_lib.bwd_workload(w, alpha=alpha)
+    dy = w.dy.double().numpy()
+
+    def loss(q, k):
+        r = oracle_lib.fwd(q, k, w.v, w.u, w.seq_offsets, N, w.pos_w, w.time_w,
+                           w.timestamps, w.num_buckets, alpha=alpha)
+        return float((r["y"] * dy).sum())
+    h = 1e-6
+    rng = np.random.default_rng(3)
+    for name, gname in (("q", "dq"), ("k", "dk")):
+        base = getattr(w, name).double().clone()
+        flat = base.view(-1)
+        for ix in rng.choice(flat.numel(), size=8, replace=False):
+            p = flat.clone(); p[ix] += h
+            m = flat.clone(); m[ix] -= h
+            args_p = (p.view(base.shape), w.k) if name == "q" else (w.q, p.view(base.shape))
+            args_m = (m.view(base.shape), w.k) if name == "q" else (w.q, m.view(base.shape))
+            fd = (loss(*args_p) - loss(*args_m)) / (2 * h)
+            an = float(g[gname].reshape(-1)[ix])
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, ix, fd, an)
