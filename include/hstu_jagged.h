@@ -11,7 +11,7 @@
  * encodings) this library computes, for every sequence b with rows
  * off[b] .. off[b+1]-1, every head h and local positions i, j:
  *
- *   s_ij = <q_i, k_j> + pos_w[h, j - i + N - 1] + time_w[h, bucket(ts_i - ts_j)]
+ *   s_ij = alpha <q_i, k_j> + pos_w[h, j - i + N - 1] + time_w[h, bucket(ts_i - ts_j)]
  *   a_ij = silu(s_ij) / N   for j <= i (causal), else 0;   N = max_len
  *   o_i  = sum_j a_ij v_j                                    (per head)
  *   y    = LayerNorm(o) * u   per token over all H*d features
@@ -22,8 +22,9 @@
  * buckets per octave; the paper names bucketized time encodings without
  * giving the rule, this is the library's reading).
  *
- * The backward pass returns dq, dk, dv, du and the table gradients d_pos_w,
- * d_time_w of sum(y * dy).
+ * with alpha = 1 unless hstu_rab.alpha says otherwise.  The backward pass
+ * returns dq, dk, dv, du and the table gradients d_pos_w, d_time_w of
+ * sum(y * dy).
  *
  * Layout.  Every tensor is row-major and contiguous.  q, k, v, u, o, dq, dk,
  * dv, du and dO are [T][H][d]; y and dy are [T][H*d] (the same memory
@@ -98,6 +99,11 @@ typedef struct {
     const int64_t *timestamps;   /* [T] int64; required iff time_w != NULL   */
     int32_t num_buckets;         /* >= 1 iff time_w != NULL; H*num_buckets
                                     <= 4096 for HSTU_BF16                     */
+    float alpha;                 /* scale of <q_i, k_j>: s_ij = alpha <q_i, k_j>
+                                    + biases (one of the RAB variants of Sec.
+                                    4.1.1's operator); 0 is read as 1, so a
+                                    zero-initialised struct is the plain
+                                    operator; must be finite               */
 } hstu_rab;
 
 /* Forward outputs and scratch, all caller-allocated.  o, ln_mean and
@@ -129,6 +135,17 @@ typedef struct {
     float *d_time_w;             /* [H][num_buckets]; required iff time_w    */
     void *workspace;             /* device scratch, 256-byte aligned         */
     size_t workspace_bytes;      /* >= hstu_jagged_attn_workspace_bytes(..,1) */
+    int32_t deterministic;       /* nonzero: bitwise reproducible table
+                                    gradients.  Every partial sum of d_pos_w
+                                    and d_time_w is then kept in 64-bit fixed
+                                    point (resolution 2^-32 of N dS, so
+                                    |partial sums of N dS| < 2^31 is
+                                    required) and added with integer atomics,
+                                    whose result does not depend on order;
+                                    dq, dk, dv, du are reproducible either
+                                    way.  0: floating-point accumulation
+                                    (faster; the last bits of the tables may
+                                    differ from run to run)                  */
 } hstu_bwd_io;
 
 /* Forward: o, y, ln_mean, ln_rstd from q, k, v, u (Sec. 4.1.1). */

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -77,6 +78,10 @@ int validate(const void *q, const void *k, const void *v, const void *u,
   const char *chk = getenv("HSTU_VALIDATE");
   p->check_offsets = chk && chk[0] == '1';
   p->has_pos = has_pos; p->has_time = has_time; p->nb = nb;
+  float alpha = rab ? rab->alpha : 0.0f;
+  if (!std::isfinite(alpha)) return fail(HSTU_EINVAL, "rab->alpha is not finite");
+  p->alpha = alpha == 0.0f ? 1.0f : alpha;
+  p->deterministic = false;
   // sum_b ceil(L_b/64) <= min(B * ceil(N/64), floor((T + 63 B) / 64))
   p->max_entries = std::min<int64_t>((int64_t)B * ceil_div(N, TILE),
                                      (T + (int64_t)(TILE - 1) * B) / TILE);
@@ -195,10 +200,21 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   // each kind runs at its own occupancy.
   L.bwd_combined = bf16_bwd && p.max_entries * p.H < (int64_t)BWD_COMBINED_ITEMS_PER_WG *
                                                       std::max(L.bwd_grid_both, 1);
-  L.dpos_part = (bf16_bwd && p.has_pos) ? take(sizeof(float) * (size_t)p.T * p.H) : 0;
-  L.dtime_part = (bf16_bwd && p.has_time)
-                     ? take(sizeof(float) * (size_t)DTIME_BINS * p.H * p.nb)
-                     : 0;
+  // Table-gradient partials: 8 bytes per entry, which the deterministic
+  // backward uses as 64-bit fixed point and the default one as float (in
+  // the first half).  bf16: per-sequence diagonal partials and DTIME_BINS
+  // histograms; fp32: one table-shaped fixed-point staging buffer each
+  // (used by the deterministic mode only).
+  const bool f32_bwd = for_bwd && p.dtype == HSTU_F32;
+  const size_t span = 2 * (size_t)p.N - 1;
+  L.dpos_part = !p.has_pos ? 0
+                : bf16_bwd ? take(sizeof(int64_t) * (size_t)p.T * p.H)
+                : f32_bwd  ? take(sizeof(int64_t) * span * p.H)
+                           : 0;
+  L.dtime_part = !p.has_time ? 0
+                 : bf16_bwd ? take(sizeof(int64_t) * (size_t)DTIME_BINS * p.H * p.nb)
+                 : f32_bwd  ? take(sizeof(int64_t) * (size_t)p.H * p.nb)
+                            : 0;
   L.total = at;
   return L;
 }
@@ -344,6 +360,7 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
   if (p.has_time && !io->d_time_w)
     return fail(HSTU_EINVAL, "rab->time_w given but io->d_time_w is NULL");
   if (p.T == 0 && !p.has_pos && !p.has_time) return HSTU_OK;
+  p.deterministic = io->deterministic != 0;
   int dev = 0;
   if ((rc = current_device(&dev)) != HSTU_OK) return rc;
   Layout L = make_layout(p, true, dev);
@@ -363,7 +380,8 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
     // the LayerNorm backward launch also builds the work lists
     prof::Scope ps("ln_bwd", s);
     e = launch_ln_bwd_sched(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
-                            ws + L.dO, L.dpos_part ? (float *)(ws + L.dpos_part) : nullptr,
+                            ws + L.dO,
+                            (L.dpos_part && p.dtype == HSTU_BF16) ? ws + L.dpos_part : nullptr,
                             seq_offsets, ws, L, s);
     if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
   } else {

@@ -77,9 +77,13 @@ struct KParams {
   const WorkEntry *list;
   u16 *out0, *out1;
   u16 *dq_out;
-  float *dpos_part, *dtime_part;
+  void *dpos_part, *dtime_part;        // float, or fixed point (deterministic)
   int32_t H, N, nb;
   float inv_n;
+  // scale of <q, k>: the forward works on x' = s alpha log2e with the biases
+  // staged pre-scaled, the backward on s/alpha-scaled biases (inv_alpha)
+  float alpha, inv_alpha, neg_al2e;
+  float dqk_scale;                     // alpha / N: dQ and dK stores
   int32_t all_heads;      // time tables of every head staged once per work-group
   int32_t fuse_dq0;       // combined backward, d=64: the dK/dV items of first
                           // k-tiles compute their q-tile's dQ (no such dQ items)
@@ -393,7 +397,7 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
     ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, 1.0f);
+  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, P.inv_alpha);
 }
 
 // ---------------------------------------------------------------- forward
@@ -504,7 +508,7 @@ attn_fwd_kernel(KParams P) {
         dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, P.inv_alpha);
       } else if (has_next) {   // ... or the next item's first one
         fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
                                      tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
@@ -535,14 +539,16 @@ attn_fwd_kernel(KParams P) {
         load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
                            i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
 
-      // x' = (s + pos) log2e + time bias', A = silu(x)/N, then O_wi += A V,
-      // one 16-key half at a time (half the temporaries live at once)
+      // x' = (s + pos/alpha) alpha log2e + time bias', A = silu(x)/N, then
+      // O_wi += A V, one 16-key half at a time (half the temporaries live at
+      // once)
       const float nl = (float)P.N * L2E;
+      const float al2e = P.alpha * L2E;
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         float x[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e] * L2E;
+        for (int e = 0; e < 8; ++e) x[e] = s[8 * hh + e] * al2e;
         if (TIME) {
           if (!slow) {
 #pragma unroll
@@ -684,18 +690,20 @@ struct StreamSmem {
 // to its bucket of the work-group's histogram `hist`.  A run is opened by
 // the first index of the item's first tile (start), so adding needs no test
 // for an empty run.
+template <typename A>
 struct TimeRun {
+  typedef typename A::L L;
   float sum = 0.0f;
   int cur = -1;
   __device__ __forceinline__ void start(int k) { cur = cur < 0 ? k : cur; }
-  __device__ __forceinline__ void add(double *hist, int nb, int k, float v) {
+  __device__ __forceinline__ void add(L *hist, int nb, int k, float v) {
     const bool change = k != cur;
-    if (change) atomicAdd(&hist[bucket_of_index(cur, nb)], (double)sum);
+    if (change) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum));
     sum = change ? v : sum + v;
     cur = k;
   }
-  __device__ __forceinline__ void flush(double *hist, int nb) {
-    if (cur >= 0) atomicAdd(&hist[bucket_of_index(cur, nb)], (double)sum);
+  __device__ __forceinline__ void flush(L *hist, int nb) {
+    if (cur >= 0) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum));
     cur = -1;
     sum = 0.0f;
   }
@@ -710,6 +718,22 @@ __device__ __forceinline__ float dsilu(float x) {
   const float sg = sigmoid_f(x);
   return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f);
 }
+
+// Table-gradient accumulation types: LDS sums in double and global partials
+// in float, or (deterministic mode) both as 64-bit fixed point, whose
+// integer additions give the same result in any order.
+template <bool DET> struct TabAcc {
+  typedef double L;
+  typedef float G;
+  static __device__ __forceinline__ L lds(float v) { return (double)v; }
+  static __device__ __forceinline__ G glob(L v) { return (float)v; }
+};
+template <> struct TabAcc<true> {
+  typedef unsigned long long L;
+  typedef unsigned long long G;
+  static __device__ __forceinline__ L lds(float v) { return to_fix(v); }
+  static __device__ __forceinline__ G glob(L v) { return v; }
+};
 
 // The backward kernels' persistent loop: a work-group's first item is
 // static (its block index in the longest-first list) and every item pops the
@@ -773,7 +797,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       ts_i = P.ts[si.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
       if (tid < TILE) ts_k = P.ts[si.start + (tid < si.len ? tid : si.len - 1)];
     }
-    float pos_v = POS ? pos_fetch(P, h, qt, 0, tid, 1.0f) : 0.0f;
+    float pos_v = POS ? pos_fetch(P, h, qt, 0, tid, P.inv_alpha) : 0.0f;
 
     float ts_i32 = 0.0f;
     bool q_far = false;
@@ -781,11 +805,11 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     if (TIME) {
       // the work-group's tables, staged at its first item after that item's
       // loads (both latencies overlap)
-      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, 1.0f);
+      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, P.inv_alpha);
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid, 1.0f);
+      ktab = item_time_slot(P, dyn, h, tid, P.inv_alpha);
     }
 
     f32x16 acc[D / 32];
@@ -819,7 +843,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         if (TIME && tid < TILE) ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, 1.0f);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, P.inv_alpha);
       }
 
       // S^T quadrant with the position bias as the accumulator's initial
@@ -866,13 +890,16 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
               x[e] += ktab[KTAB + time_bucket(ts_i - sm.ts64[kb + c_row(8 * hh + e, 0)], P.nb)];
           }
         }
+        // the score is alpha x: sigma(alpha x), silu'(alpha x) =
+        // sigma (1 + x (alpha - alpha sigma))
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * -L2E);
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * P.neg_al2e);
 #pragma unroll
         for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_rcpf(1.0f + sg[e]);
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          dsv[e] = (sg[e] * da[8 * hh + e]) * __builtin_fmaf(x[e], 1.0f - sg[e], 1.0f);
+          dsv[e] = (sg[e] * da[8 * hh + e]) *
+                   __builtin_fmaf(x[e], __builtin_fmaf(-P.alpha, sg[e], P.alpha), 1.0f);
         if (kt == qt) {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
@@ -892,7 +919,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     }
 
     sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
-                      row_stride, q_valid, P.inv_n);
+                      row_stride, q_valid, P.dqk_scale);
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -906,10 +933,10 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
 // final (no later tile pair reaches those diagonals) and go to the
 // sequence's global partial, slots x >= 64 carry into slot x - 64 of the
 // current window, and the previous window is cleared for reuse.
-template <int D, bool POS>
+template <int D, bool POS, bool DET>
 struct DkvSmem {
   StreamSmem<D> s;
-  double pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
+  typename TabAcc<DET>::L pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
   // At d=64 the item's stationary K and V tiles live here (swizzled, filled
   // by global-to-LDS loads) instead of in registers, which lets the kernel
   // run three waves per SIMD.
@@ -921,19 +948,21 @@ struct DkvSmem {
 // the two copies are summed and cleared; a final diagonal m is returned
 // through (dst, val) for a deferred global atomic into dp[m * H] (dp: this
 // sequence's and head's partials), a carried one is added into `cur`.
-__device__ __forceinline__ void dpos_retire(double (*prev)[2 * TILE], double (*cur)[2 * TILE],
-                                            int x, int dt, bool last, int len, float *dp,
-                                            int H, float *&dst, float &val) {
-  const double v = prev[0][x] + prev[1][x];
-  prev[0][x] = 0.0;
-  prev[1][x] = 0.0;
+template <typename A>
+__device__ __forceinline__ void dpos_retire(typename A::L (*prev)[2 * TILE],
+                                            typename A::L (*cur)[2 * TILE], int x, int dt,
+                                            bool last, int len, typename A::G *dp, int H,
+                                            typename A::G *&dst, typename A::G &val) {
+  const typename A::L v = prev[0][x] + prev[1][x];
+  prev[0][x] = 0;
+  prev[1][x] = 0;
   if (x < TILE || last) {
     const int m = dt * TILE + x - (TILE - 1);
-    if (v != 0.0 && m >= 0 && m < len) {
+    if (v != 0 && m >= 0 && m < len) {
       dst = dp + m * H;
-      val = (float)v;
+      val = A::glob(v);
     }
-  } else if (v != 0.0) {
+  } else if (v != 0) {
     atomicAdd(&cur[0][x - TILE], v);
   }
 }
@@ -957,11 +986,14 @@ __device__ __forceinline__ f32x16 dq0_block(const u16 *dsb, const u16 *kst, int 
 // One k-stationary item: dV_j, dK_j for a 64-row key tile of one head over
 // its query tiles, with the table gradients (d_pos through the sheared tile
 // and the rolling diagonal window, d_time through per-lane index runs).
-template <int D, bool POS, bool TIME>
-__device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx, float *dyn,
-                                         double *tacc, const int tid0, const WorkEntry e,
-                                         const int h, int &phase, float *&pend_p,
-                                         float &pend_v, int &nxt, u16 *dsb = nullptr) {
+template <int D, bool POS, bool TIME, bool DET>
+__device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> &smx,
+                                         float *dyn, typename TabAcc<DET>::L *tacc,
+                                         const int tid0, const WorkEntry e, const int h,
+                                         int &phase, typename TabAcc<DET>::G *&pend_p,
+                                         typename TabAcc<DET>::G &pend_v, int &nxt,
+                                         u16 *dsb = nullptr) {
+  typedef TabAcc<DET> A;
   constexpr int ST = D + RM_PAD;
   StreamSmem<D> &sm = smx.s;
     int tid = tid0;
@@ -1010,21 +1042,21 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
       ts_j = P.ts[r0k + (j_loc < k_valid ? j_loc : k_valid - 1)];
       if (tid < TILE) ts_q = P.ts[r0k + (tid < k_valid ? tid : k_valid - 1)];
     }
-    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, 1.0f) : 0.0f;
+    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, P.inv_alpha) : 0.0f;
 
     float ts_j32 = 0.0f;
     bool k_far = false;
     float *ktab = dyn;
     if (TIME) {
-      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, 1.0f);   // as in dq_item
+      if (phase == 0) stage_all_heads<D == 64 ? 8 : 1>(P, dyn, tid, P.inv_alpha);   // as in dq_item
       const int64_t rel = ts_j - ts_start;
       ts_j32 = (float)(int32_t)rel;
       k_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid, 1.0f);
+      ktab = item_time_slot(P, dyn, h, tid, P.inv_alpha);
     }
-    TimeRun run;                              // fast path: by float-exponent index
-    double *my_t = TIME ? tacc + h * P.nb : nullptr;
-    float *dp_item = POS ? P.dpos_part + si.start * P.H + h : nullptr;
+    TimeRun<A> run;                           // fast path: by float-exponent index
+    typename A::L *my_t = TIME ? tacc + h * P.nb : nullptr;
+    typename A::G *dp_item = POS ? (typename A::G *)P.dpos_part + si.start * P.H + h : nullptr;
 
     f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -1042,8 +1074,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         if (pend_p) atomicAdd(pend_p, pend_v);
         pend_p = nullptr;
         if (qt > kt && tid < 2 * TILE - 1) {
-          dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid, qt - 1 - kt,
-                      false, si.len, dp_item, P.H, pend_p, pend_v);
+          dpos_retire<A>(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid, qt - 1 - kt,
+                         false, si.len, dp_item, P.H, pend_p, pend_v);
           if (pend_p) atomicAdd(pend_p, pend_v);
           pend_p = nullptr;
         }
@@ -1068,7 +1100,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
         dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
         if (TIME && tid < TILE) ts_q = P.ts[r0 + (tid < nv ? tid : nv - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, 1.0f);
+        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, P.inv_alpha);
       }
 
       // this lane's queries sit at ib + 8 q4 + c, ib = 32 wi + 4 g; offset
@@ -1136,13 +1168,14 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
             }
           }
         }
+        // the score is alpha x (biases staged divided by alpha)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * -L2E);
+        for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_exp2f(x[e] * P.neg_al2e);
 #pragma unroll
         for (int e = 0; e < 8; ++e) sg[e] = __builtin_amdgcn_rcpf(1.0f + sg[e]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float a1 = x[e] * sg[e];
+          const float a1 = (P.alpha * x[e]) * sg[e];
           av[e] = a1;
           dsv[e] = da[8 * hh + e] * __builtin_fmaf(-a1, sg[e], sg[e] + a1);
         }
@@ -1153,9 +1186,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
         }
         if constexpr (POS) {
           // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0)
-          double *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
+          typename A::L *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) atomicAdd(pw + c_row(8 * hh + e, 0), (double)dsv[e]);
+          for (int e = 0; e < 8; ++e) atomicAdd(pw + c_row(8 * hh + e, 0), A::lds(dsv[e]));
         }
         if (TIME) {
           // slow tiles accumulate by bucket straight into the work-group
@@ -1171,7 +1204,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
               // conversion would keep the doubles live across this branch
               float v = dsv[e];
               asm volatile("" : "+v"(v));
-              if (v != 0.0f) atomicAdd(&my_t[tk[e]], (double)v);
+              if (v != 0.0f) atomicAdd(&my_t[tk[e]], A::lds(v));
             }
           }
         }
@@ -1205,16 +1238,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
     lds_barrier();
     if constexpr (POS) {   // every diagonal of the last window is final
       if (tid < 2 * TILE - 1)
-        dpos_retire(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid,
-                    si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
+        dpos_retire<A>(smx.pwin[(phase - 1) & 1], smx.pwin[phase & 1], tid,
+                       si.ntiles - 1 - kt, true, si.len, dp_item, P.H, pend_p, pend_v);
     }
     if constexpr (KV_LDS) {
       if (with_dq)
         quad_store_tile<D>(&sm.red[0][0], dq0_block<D>(dsb, smx.kst, wi, wj, g, lane), wi, wj,
-                           g, l32, tid, P.dq_out + koff, row_stride, k_valid, P.inv_n);
+                           g, l32, tid, P.dq_out + koff, row_stride, k_valid, P.dqk_scale);
     }
     sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
-                      row_stride, k_valid, P.inv_n);
+                      row_stride, k_valid, P.dqk_scale);
     sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
                       row_stride, k_valid, P.inv_n);
 }
@@ -1222,54 +1255,59 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS> &smx,
 // Work-group start of the kernels that run dK/dV items: zeroed d_time
 // histogram, cleared flags and d_pos windows (the
 // time tables are staged by the first item).
-template <int D, bool POS, bool TIME>
-__device__ __forceinline__ void dkv_kernel_init(const KParams &P, DkvSmem<D, POS> &smx,
-                                                double *tacc, float *dyn, int tid0) {
+template <int D, bool POS, bool TIME, bool DET>
+__device__ __forceinline__ void dkv_kernel_init(const KParams &P, DkvSmem<D, POS, DET> &smx,
+                                                typename TabAcc<DET>::L *tacc, float *dyn,
+                                                int tid0) {
   if (TIME) {
-    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0.0;
+    for (int x = tid0; x < P.H * P.nb; x += THREADS) tacc[x] = 0;
   }
   if (tid0 < 2) smx.s.flag[tid0] = 0;
   if constexpr (POS)
-    for (int x = tid0; x < 2 * 2 * 2 * TILE; x += THREADS) (&smx.pwin[0][0][0])[x] = 0.0;
+    for (int x = tid0; x < 2 * 2 * 2 * TILE; x += THREADS) (&smx.pwin[0][0][0])[x] = 0;
 }
 
 // Work-group end: the last deferred d_pos sum (a finished diagonal is sent
 // one tile later, after the next wait for the prefetched tiles, because that
 // wait also counts atomics), then this work-group's d_time histogram folded
 // into one of DTIME_BINS partials.
-template <int D, bool POS, bool TIME>
-__device__ __forceinline__ void dkv_kernel_fini(const KParams &P, double *tacc, int tid0,
-                                                float *pend_p, float pend_v) {
+template <int D, bool POS, bool TIME, bool DET>
+__device__ __forceinline__ void dkv_kernel_fini(const KParams &P, typename TabAcc<DET>::L *tacc,
+                                                int tid0, typename TabAcc<DET>::G *pend_p,
+                                                typename TabAcc<DET>::G pend_v) {
+  typedef TabAcc<DET> A;
   if (POS && pend_p) atomicAdd(pend_p, pend_v);
   if (TIME) {
     lds_barrier();
-    float *part = P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
+    typename A::G *part =
+        (typename A::G *)P.dtime_part + (int64_t)(blockIdx.x % DTIME_BINS) * P.H * P.nb;
     for (int x = tid0; x < P.H * P.nb; x += THREADS)
-      if (tacc[x] != 0.0) atomicAdd(&part[x], (float)tacc[x]);
+      if (tacc[x] != 0) atomicAdd(&part[x], A::glob(tacc[x]));
   }
 }
 
 // Backward, both item kinds in one launch over the combined list, whose
 // entries are dK/dV items (k-stationary) and dQ items (flagged,
 // q-stationary) in one longest-first order.
-template <int D, bool POS, bool TIME>
+template <int D, bool POS, bool TIME, bool DET>
 __global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
 attn_bwd_kernel(KParams P) {
-  __shared__ DkvSmem<D, POS> smx;
+  typedef TabAcc<DET> A;
+  __shared__ DkvSmem<D, POS, DET> smx;
   // dS^T of a first tile pair (d=64, see dkv_item)
   __shared__ __attribute__((aligned(16))) u16 dsb[D == 64 ? TILE * DS_STRIDE : 8];
   StreamSmem<D> &sm = smx.s;
   // dynamic LDS: [H][nb] d_time (double), then the time tables
   extern __shared__ double dyn_k[];
-  double *tacc = dyn_k;
+  typename A::L *tacc = (typename A::L *)dyn_k;
   float *dyn = (float *)(dyn_k + P.H * P.nb);
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_BWD] * P.H;
-  dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
+  dkv_kernel_init<D, POS, TIME, DET>(P, smx, tacc, dyn, tid0);
   lds_barrier();
   int phase = 0;
-  float *pend_p = nullptr;
-  float pend_v = 0.0f;
+  typename A::G *pend_p = nullptr;
+  typename A::G pend_v = 0;
   int nxt = 0;
   for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt)) {
     WorkEntry e = P.list[item / P.H];
@@ -1278,11 +1316,11 @@ attn_bwd_kernel(KParams P) {
       e.tile &= ~BWD_DQ_FLAG;
       dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase, nxt);
     } else {
-      dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt,
-                             P.fuse_dq0 ? dsb : nullptr);
+      dkv_item<D, POS, TIME, DET>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt,
+                                  P.fuse_dq0 ? dsb : nullptr);
     }
   }
-  dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
+  dkv_kernel_fini<D, POS, TIME, DET>(P, tacc, tid0, pend_p, pend_v);
 }
 
 // Backward, dQ: persistent work-groups pop q-tile items longest first.
@@ -1303,26 +1341,27 @@ attn_bwd_dq_kernel(KParams P) {
 
 // Backward, dK/dV and the table gradients: persistent work-groups pop k-tile
 // items longest first.
-template <int D, bool POS, bool TIME>
+template <int D, bool POS, bool TIME, bool DET>
 __global__ void __launch_bounds__(THREADS, D == 64 ? (TIME ? 2 : 3) : 1)
 attn_bwd_dkv_kernel(KParams P) {
-  __shared__ DkvSmem<D, POS> smx;
+  typedef TabAcc<DET> A;
+  __shared__ DkvSmem<D, POS, DET> smx;
   StreamSmem<D> &sm = smx.s;
   extern __shared__ double dyn_k[];
-  double *tacc = dyn_k;
+  typename A::L *tacc = (typename A::L *)dyn_k;
   float *dyn = (float *)(dyn_k + P.H * P.nb);
   const int tid0 = threadIdx.x;
   const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
-  dkv_kernel_init<D, POS, TIME>(P, smx, tacc, dyn, tid0);
+  dkv_kernel_init<D, POS, TIME, DET>(P, smx, tacc, dyn, tid0);
   lds_barrier();
   int phase = 0;
-  float *pend_p = nullptr;
-  float pend_v = 0.0f;
+  typename A::G *pend_p = nullptr;
+  typename A::G pend_v = 0;
   int nxt = 0;
   for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt))
-    dkv_item<D, POS, TIME>(P, smx, dyn, tacc, tid0, P.list[item / P.H], item % P.H, phase,
-                           pend_p, pend_v, nxt);
-  dkv_kernel_fini<D, POS, TIME>(P, tacc, tid0, pend_p, pend_v);
+    dkv_item<D, POS, TIME, DET>(P, smx, dyn, tacc, tid0, P.list[item / P.H], item % P.H,
+                                phase, pend_p, pend_v, nxt);
+  dkv_kernel_fini<D, POS, TIME, DET>(P, tacc, tid0, pend_p, pend_v);
 }
 
 // ------------------------------------------------------------- launchers
@@ -1369,6 +1408,10 @@ KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
   P.N = a.p.N;
   P.nb = a.p.has_time ? a.p.nb : 0;
   P.inv_n = 1.0f / (float)a.p.N;
+  P.alpha = a.p.alpha;
+  P.inv_alpha = 1.0f / a.p.alpha;
+  P.neg_al2e = -a.p.alpha * L2E;
+  P.dqk_scale = a.p.alpha / (float)a.p.N;
   P.all_heads = all_heads(a.p) ? 1 : 0;
   return P;
 }
@@ -1386,6 +1429,37 @@ KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
       else if (TIME) { auto kfn = KERNEL<128, false, true>; __VA_ARGS__; }   \
       else { auto kfn = KERNEL<128, false, false>; __VA_ARGS__; }            \
     }                                                                         \
+  } while (0)
+
+// As HSTU_DISPATCH, for the kernels that accumulate the table gradients
+// (a fourth template argument: the deterministic fixed-point mode).
+#define HSTU_DISPATCH_TAB(KERNEL, D, POS, TIME, DET, ...)                             \
+  do {                                                                                \
+    if (DET) {                                                                        \
+      if (D == 64) {                                                                  \
+        if (POS && TIME) { auto kfn = KERNEL<64, true, true, true>; __VA_ARGS__; }    \
+        else if (POS) { auto kfn = KERNEL<64, true, false, true>; __VA_ARGS__; }     \
+        else if (TIME) { auto kfn = KERNEL<64, false, true, true>; __VA_ARGS__; }    \
+        else { auto kfn = KERNEL<64, false, false, true>; __VA_ARGS__; }             \
+      } else {                                                                        \
+        if (POS && TIME) { auto kfn = KERNEL<128, true, true, true>; __VA_ARGS__; }   \
+        else if (POS) { auto kfn = KERNEL<128, true, false, true>; __VA_ARGS__; }    \
+        else if (TIME) { auto kfn = KERNEL<128, false, true, true>; __VA_ARGS__; }   \
+        else { auto kfn = KERNEL<128, false, false, true>; __VA_ARGS__; }            \
+      }                                                                               \
+    } else {                                                                          \
+      if (D == 64) {                                                                  \
+        if (POS && TIME) { auto kfn = KERNEL<64, true, true, false>; __VA_ARGS__; }   \
+        else if (POS) { auto kfn = KERNEL<64, true, false, false>; __VA_ARGS__; }    \
+        else if (TIME) { auto kfn = KERNEL<64, false, true, false>; __VA_ARGS__; }   \
+        else { auto kfn = KERNEL<64, false, false, false>; __VA_ARGS__; }            \
+      } else {                                                                        \
+        if (POS && TIME) { auto kfn = KERNEL<128, true, true, false>; __VA_ARGS__; }  \
+        else if (POS) { auto kfn = KERNEL<128, true, false, false>; __VA_ARGS__; }   \
+        else if (TIME) { auto kfn = KERNEL<128, false, true, false>; __VA_ARGS__; }  \
+        else { auto kfn = KERNEL<128, false, false, false>; __VA_ARGS__; }           \
+      }                                                                               \
+    }                                                                                 \
   } while (0)
 
 int current_dev() {
@@ -1406,8 +1480,8 @@ int attn_fwd_grid(const Problem &p, int dev) {
 
 int attn_bwd_grid(const Problem &p, int dev) {
   int grid = 1;
-  HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, k_dyn_bytes(p), 2 * p.max_entries * p.H, dev));
+  HSTU_DISPATCH_TAB(attn_bwd_kernel, p.d, p.has_pos, p.has_time, p.deterministic,
+                    grid = persistent_grid(kfn, k_dyn_bytes(p), 2 * p.max_entries * p.H, dev));
   return grid;
 }
 
@@ -1420,8 +1494,8 @@ int attn_bwd_dq_grid(const Problem &p, int dev) {
 
 int attn_bwd_dkv_grid(const Problem &p, int dev) {
   int grid = 1;
-  HSTU_DISPATCH(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, k_dyn_bytes(p), p.max_entries * p.H, dev));
+  HSTU_DISPATCH_TAB(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time, p.deterministic,
+                    grid = persistent_grid(kfn, k_dyn_bytes(p), p.max_entries * p.H, dev));
   return grid;
 }
 
@@ -1449,13 +1523,13 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
     P.out0 = (u16 *)dk;
     P.out1 = (u16 *)dv;
     P.dq_out = (u16 *)dq;
-    P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
-    P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
+    P.dpos_part = a.L.dpos_part ? (void *)(ws + a.L.dpos_part) : nullptr;
+    P.dtime_part = a.L.dtime_part ? (void *)(ws + a.L.dtime_part) : nullptr;
     // must match the scheduler's choice (sched_args)
     P.fuse_dq0 = p.d == 64 ? 1 : 0;
-    HSTU_DISPATCH(attn_bwd_kernel, p.d, p.has_pos, p.has_time,
-                  hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_both), dim3(THREADS),
-                                     k_dyn_bytes(p), s, P));
+    HSTU_DISPATCH_TAB(attn_bwd_kernel, p.d, p.has_pos, p.has_time, p.deterministic,
+                      hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_both), dim3(THREADS),
+                                         k_dyn_bytes(p), s, P));
     return hipGetLastError();
   }
   {
@@ -1465,11 +1539,11 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
     P.dO = (const u16 *)dO;
     P.out0 = (u16 *)dk;
     P.out1 = (u16 *)dv;
-    P.dpos_part = a.L.dpos_part ? (float *)(ws + a.L.dpos_part) : nullptr;
-    P.dtime_part = a.L.dtime_part ? (float *)(ws + a.L.dtime_part) : nullptr;
-    HSTU_DISPATCH(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time,
-                  hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_dkv), dim3(THREADS),
-                                     k_dyn_bytes(p), s, P));
+    P.dpos_part = a.L.dpos_part ? (void *)(ws + a.L.dpos_part) : nullptr;
+    P.dtime_part = a.L.dtime_part ? (void *)(ws + a.L.dtime_part) : nullptr;
+    HSTU_DISPATCH_TAB(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time, p.deterministic,
+                      hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_dkv), dim3(THREADS),
+                                         k_dyn_bytes(p), s, P));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -5,7 +5,9 @@
 // row of the 64-row tile (a query for the forward and dQ, a key for dK/dV)
 // and walks its causal partners; every thread of a wave reads the same
 // partner row at the same time, so those loads are broadcasts.  Table
-// gradients are float atomics straight into the (zeroed) outputs.  This path
+// gradients are float atomics straight into the (zeroed) outputs, or, in the
+// deterministic mode, 64-bit fixed-point atomics into workspace tables that a
+// last pass converts (integer sums do not depend on order).  This path
 // serves the fp32 workload and precision checks; it is not the throughput
 // path.
 #include "internal.h"
@@ -26,8 +28,9 @@ struct F32Params {
   const WorkEntry *list;
   float *out0, *out1, *out2;
   float *d_pos, *d_time;
+  unsigned long long *fix_pos, *fix_time;   // deterministic mode: fixed-point sums
   int32_t H, N, nb;
-  float inv_n;
+  float inv_n, alpha;
 };
 
 __device__ __forceinline__ float bias(const F32Params &P, int h, int64_t i,
@@ -61,7 +64,7 @@ f32_fwd_kernel(F32Params P) {
     float s = 0.0f;
 #pragma unroll
     for (int c = 0; c < D; ++c) s = fmaf(qi[c], kj[c], s);
-    s += bias(P, h, i, j, ri, rj);
+    s = P.alpha * s + bias(P, h, i, j, ri, rj);
     const float a = s * sigmoid_f(s) * P.inv_n;
 #pragma unroll
     for (int c = 0; c < D; ++c) acc[c] = fmaf(a, vj[c], acc[c]);
@@ -97,14 +100,14 @@ f32_dq_kernel(F32Params P) {
       s = fmaf(qi[c], kj[c], s);
       da = fmaf(doi[c], vj[c], da);
     }
-    s += bias(P, h, i, j, ri, rj);
+    s = P.alpha * s + bias(P, h, i, j, ri, rj);
     const float sg = sigmoid_f(s);
     const float ds = da * sg * (1.0f + s * (1.0f - sg)) * P.inv_n;
 #pragma unroll
     for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, kj[c], acc[c]);
   }
 #pragma unroll
-  for (int c = 0; c < D; ++c) P.out0[(ri * P.H + h) * D + c] = acc[c];
+  for (int c = 0; c < D; ++c) P.out0[(ri * P.H + h) * D + c] = P.alpha * acc[c];
 }
 
 template <int D>
@@ -135,7 +138,7 @@ f32_dkv_kernel(F32Params P) {
       s = fmaf(qi[c], kj[c], s);
       da = fmaf(doi[c], vj[c], da);
     }
-    s += bias(P, h, i, j, ri, rj);
+    s = P.alpha * s + bias(P, h, i, j, ri, rj);
     const float sg = sigmoid_f(s);
     const float a = s * sg * P.inv_n;
     const float ds = da * sg * (1.0f + s * (1.0f - sg)) * P.inv_n;
@@ -144,13 +147,18 @@ f32_dkv_kernel(F32Params P) {
       dv[c] = fmaf(a, doi[c], dv[c]);
       dk[c] = fmaf(ds, qi[c], dk[c]);
     }
-    if (P.d_pos) atomicAdd(&P.d_pos[(int64_t)h * (2 * (int64_t)P.N - 1) + (j - i + P.N - 1)], ds);
-    if (P.d_time)
-      atomicAdd(&P.d_time[(int64_t)h * P.nb + time_bucket(P.ts[ri] - P.ts[rj], P.nb)], ds);
+    const int64_t xp = (int64_t)h * (2 * (int64_t)P.N - 1) + (j - i + P.N - 1);
+    if (P.d_pos) atomicAdd(&P.d_pos[xp], ds);
+    if (P.fix_pos) atomicAdd(&P.fix_pos[xp], to_fix(ds));
+    if (P.d_time || P.fix_time) {
+      const int64_t xt = (int64_t)h * P.nb + time_bucket(P.ts[ri] - P.ts[rj], P.nb);
+      if (P.d_time) atomicAdd(&P.d_time[xt], ds);
+      if (P.fix_time) atomicAdd(&P.fix_time[xt], to_fix(ds));
+    }
   }
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    P.out1[(rj * P.H + h) * D + c] = dk[c];
+    P.out1[(rj * P.H + h) * D + c] = P.alpha * dk[c];
     P.out2[(rj * P.H + h) * D + c] = dv[c];
   }
 }
@@ -159,6 +167,13 @@ __global__ void fill_zero_kernel(float *p, int64_t n) {
   for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
        x += (int64_t)gridDim.x * blockDim.x)
     p[x] = 0.0f;
+}
+
+// Fixed-point table sums -> float tables.
+__global__ void fix_to_float_kernel(const unsigned long long *fix, float *out, int64_t n) {
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
+       x += (int64_t)gridDim.x * blockDim.x)
+    out[x] = (float)((double)(long long)fix[x] * (1.0 / FIX_ONE));
 }
 
 F32Params make_params(const AttnArgs &a, const WorkEntry *list) {
@@ -177,6 +192,7 @@ F32Params make_params(const AttnArgs &a, const WorkEntry *list) {
   P.N = a.p.N;
   P.nb = a.p.has_time ? a.p.nb : 0;
   P.inv_n = 1.0f / (float)a.p.N;
+  P.alpha = a.p.alpha;
   return P;
 }
 
@@ -203,13 +219,23 @@ hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
                                hipStream_t s) {
   const char *ws = (const char *)a.ws;
   const Problem &p = a.p;
+  const int64_t n_pos = (int64_t)p.H * (2 * (int64_t)p.N - 1), n_time = (int64_t)p.H * p.nb;
+  // deterministic mode: fixed-point staging tables in the workspace
+  unsigned long long *fix_pos =
+      (p.deterministic && d_pos) ? (unsigned long long *)(ws + a.L.dpos_part) : nullptr;
+  unsigned long long *fix_time =
+      (p.deterministic && d_time) ? (unsigned long long *)(ws + a.L.dtime_part) : nullptr;
   if (d_pos) {
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, d_pos,
-                       (int64_t)p.H * (2 * (int64_t)p.N - 1));
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, d_pos, n_pos);
+    if (fix_pos)
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, (float *)fix_pos,
+                         2 * n_pos);
   }
   if (d_time) {
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, d_time,
-                       (int64_t)p.H * p.nb);
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, d_time, n_time);
+    if (fix_time)
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, (float *)fix_time,
+                         2 * n_time);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.T == 0) return e;
@@ -223,9 +249,16 @@ hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
   K.dO = (const float *)dO;
   K.out1 = (float *)dk;
   K.out2 = (float *)dv;
-  K.d_pos = d_pos;
-  K.d_time = d_time;
+  K.d_pos = fix_pos ? nullptr : d_pos;
+  K.d_time = fix_time ? nullptr : d_time;
+  K.fix_pos = fix_pos;
+  K.fix_time = fix_time;
   HSTU_F32_DISPATCH(f32_dkv_kernel, p.d, grid, s, K);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (fix_pos)
+    hipLaunchKernelGGL(fix_to_float_kernel, dim3(64), dim3(256), 0, s, fix_pos, d_pos, n_pos);
+  if (fix_time)
+    hipLaunchKernelGGL(fix_to_float_kernel, dim3(8), dim3(256), 0, s, fix_time, d_time, n_time);
   return hipGetLastError();
 }
 

@@ -6,7 +6,16 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "internal.h"
+
 namespace hstu {
+
+// 64-bit fixed-point value of v (FIX_ONE per unit, rounded to nearest) for
+// the deterministic table-gradient sums: integer additions give the same
+// result in any order.  |v| < 2^31.
+__device__ __forceinline__ unsigned long long to_fix(float v) {
+  return (unsigned long long)(long long)__builtin_rint((double)v * FIX_ONE);
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));

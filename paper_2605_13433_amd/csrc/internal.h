@@ -19,6 +19,11 @@ constexpr int TILE = 64;
 // kernel sums the bins in a fixed order.
 constexpr int DTIME_BINS = 16;
 
+// Fixed-point unit of the deterministic backward's table-gradient partials:
+// a partial sum x of N dS is kept as the 64-bit integer round(x * FIX_ONE)
+// (resolution 2^-32, |x| < 2^31).
+constexpr double FIX_ONE = 4294967296.0;
+
 // The backward runs as one combined launch while the work list holds fewer
 // than this many (entry, head) items per persistent work-group.
 constexpr int BWD_COMBINED_ITEMS_PER_WG = 4;
@@ -66,6 +71,8 @@ struct Problem {
   int32_t nb;
   int64_t max_entries;   // upper bound on sum_b ceil(L_b / 64)
   bool check_offsets;    // HSTU_VALIDATE=1: the scheduler checks the contract
+  float alpha;           // scale of <q, k> (1 = plain operator)
+  bool deterministic;    // backward: fixed-point table accumulation
 };
 
 // Workspace carve-up; offsets in bytes from the workspace base, each region
@@ -163,7 +170,7 @@ hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
 // backward's lists (as launch_schedule) in the same launch.
 hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
                                const void *o, const float *mean, const float *rstd,
-                               void *du, void *dO, float *dpos_part,
+                               void *du, void *dO, void *dpos_part,
                                const int64_t *seq_offsets, void *ws, const Layout &L,
                                hipStream_t s);
 hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,

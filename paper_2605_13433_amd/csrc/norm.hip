@@ -115,7 +115,7 @@ __device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *
                                              const float *__restrict__ mean,
                                              const float *__restrict__ rstd,
                                              T *__restrict__ du, T *__restrict__ dO,
-                                             float *__restrict__ dpos_part, int H,
+                                             uint64_t *__restrict__ dpos_part, int H,
                                              int64_t T_tokens, int block) {
   constexpr int F = 8 * L, TPW = 64 / L;
   const int lane = threadIdx.x & 63, sub = lane % L;
@@ -146,8 +146,9 @@ __device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *
   }
   Vec8<T>::store(du + at, o_du);
   Vec8<T>::store(dO + at, o_do);
-  // the attention backward accumulates this token's d_pos partials
-  if (dpos_part && sub < H) dpos_part[r * H + sub] = 0.0f;
+  // the attention backward accumulates this token's d_pos partials (8
+  // bytes each: a float, or 64-bit fixed point in the deterministic mode)
+  if (dpos_part && sub < H) dpos_part[r * H + sub] = 0;
 }
 
 template <typename T>
@@ -197,7 +198,7 @@ __global__ void __launch_bounds__(LN_THREADS)
 ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
               const T *__restrict__ o, const float *__restrict__ mean,
               const float *__restrict__ rstd, T *__restrict__ du,
-              T *__restrict__ dO, float *__restrict__ dpos_part, int H,
+              T *__restrict__ dO, uint64_t *__restrict__ dpos_part, int H,
               int64_t T_tokens, int F, SchedArgs sa, int sched) {
   if (sched && blockIdx.x == 0) {
     __shared__ SchedSmem ssm;
@@ -253,7 +254,7 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
     Vec8<T>::store(dO + base + f0, o_do);
   }
   // the attention backward accumulates this token's d_pos partials
-  if (dpos_part && lane < H) dpos_part[r * H + lane] = 0.0f;
+  if (dpos_part && lane < H) dpos_part[r * H + lane] = 0;
 }
 
 // Table-gradient finalize, one launch with two block roles:
@@ -267,18 +268,32 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 // Summation order is fixed, so the result is deterministic given the
 // partials.  `scale` multiplies every entry (1/N: the backward kernel
 // accumulates N dS).
+// The deterministic backward keeps the partials as 64-bit fixed point
+// (FIX_ONE per unit); they are summed as integers, which no order changes,
+// and converted once.
 constexpr int FIN_THREADS = 1024;
 constexpr int FIN_WAVES = FIN_THREADS / 64;
 
+template <bool DET> struct FinAcc { typedef float T; };
+template <> struct FinAcc<true> { typedef unsigned long long T; };
+__device__ __forceinline__ float fin_value(float x) { return x; }
+__device__ __forceinline__ float fin_value(unsigned long long x) {
+  return (float)((double)(long long)x * (1.0 / FIX_ONE));
+}
+
+template <bool DET>
 __global__ void __launch_bounds__(FIN_THREADS)
 finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
-                       const float *__restrict__ pos_part, int H, int N,
+                       const void *__restrict__ pos_part_v, int H, int N,
                        float *__restrict__ d_pos, int pos_blocks,
-                       const float *__restrict__ time_part, int n_parts,
+                       const void *__restrict__ time_part_v, int n_parts,
                        int width, float *__restrict__ d_time, float scale) {
-  __shared__ float red[FIN_WAVES][64];
+  typedef typename FinAcc<DET>::T A;
+  const A *pos_part = (const A *)pos_part_v;
+  const A *time_part = (const A *)time_part_v;
+  __shared__ A red[FIN_WAVES][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  float acc = 0.0f;
+  A acc = 0;
   if ((int)blockIdx.x < pos_blocks) {
     const int chunks = (N + 63) / 64;
     const int h = blockIdx.x / chunks;
@@ -287,9 +302,9 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
       // eight sequences per step: their records, then their partials, each
       // group of loads issued together (two memory latencies per step)
       constexpr int G = 8;
-      float part[G];
+      A part[G];
 #pragma unroll
-      for (int k = 0; k < G; ++k) part[k] = 0.0f;
+      for (int k = 0; k < G; ++k) part[k] = 0;
       int b = wv;
       for (; b + (G - 1) * FIN_WAVES < B; b += G * FIN_WAVES) {
         SeqInfo si[G];
@@ -297,7 +312,7 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
         for (int k = 0; k < G; ++k) si[k] = info[b + k * FIN_WAVES];
 #pragma unroll
         for (int k = 0; k < G; ++k)
-          part[k] += si[k].len > m ? pos_part[(si[k].start + m) * H + h] : 0.0f;
+          part[k] += si[k].len > m ? pos_part[(si[k].start + m) * H + h] : (A)0;
       }
       for (; b < B; b += FIN_WAVES) {
         const SeqInfo si = info[b];
@@ -309,10 +324,10 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
     red[wv][lane] = acc;
     __syncthreads();
     if (wv == 0 && m < N) {
-      float s = 0.0f;
+      A s = 0;
       for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
       const int64_t span = 2 * (int64_t)N - 1;
-      d_pos[h * span + (N - 1 - m)] = scale * s;
+      d_pos[h * span + (N - 1 - m)] = scale * fin_value(s);
       if (N + m < span) d_pos[h * span + N + m] = 0.0f;
     }
   } else {
@@ -322,9 +337,9 @@ finalize_tables_kernel(const SeqInfo *__restrict__ info, int B,
     red[wv][lane] = acc;
     __syncthreads();
     if (wv == 0 && c < width) {
-      float s = 0.0f;
+      A s = 0;
       for (int x = 0; x < FIN_WAVES; ++x) s += red[x][lane];
-      d_time[c] = scale * s;
+      d_time[c] = scale * fin_value(s);
     }
   }
 }
@@ -376,9 +391,10 @@ hipError_t launch_ln_fwd(const Problem &p, const void *o, const void *u,
 
 hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
                                const void *o, const float *mean, const float *rstd,
-                               void *du, void *dO, float *dpos_part,
+                               void *du, void *dO, void *dpos_part_v,
                                const int64_t *seq_offsets, void *ws, const Layout &L,
                                hipStream_t s) {
+  uint64_t *dpos_part = (uint64_t *)dpos_part_v;
   const int F = p.H * p.d;
   const SchedArgs sa = sched_args(seq_offsets, p, ws, L);
   const int GL = ln_group_lanes(F);
@@ -402,11 +418,12 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
   const int width = d_time ? p.H * p.nb : 0;
   const int time_blocks = (width + 63) / 64;
   if (pos_blocks + time_blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_tables_kernel, dim3(pos_blocks + time_blocks),
+  auto kfn = p.deterministic ? finalize_tables_kernel<true> : finalize_tables_kernel<false>;
+  hipLaunchKernelGGL(kfn, dim3(pos_blocks + time_blocks),
                      dim3(FIN_THREADS), 0, s, (const SeqInfo *)(ws + a.L.seqinfo), p.B,
-                     d_pos ? (const float *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
+                     d_pos ? (const void *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
                      d_pos, pos_blocks,
-                     d_time ? (const float *)(ws + a.L.dtime_part) : nullptr,
+                     d_time ? (const void *)(ws + a.L.dtime_part) : nullptr,
                      DTIME_BINS, width, d_time, 1.0f / (float)p.N);
   return hipGetLastError();
 }

@@ -216,7 +216,9 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.fuse_dq0 = L.list_b && L.bwd_combined && p.d == 64 ? 1 : 0;
   a.check = p.check_offsets ? 1 : 0;
   a.zero_out = L.dtime_part ? (float *)(base + L.dtime_part) : nullptr;
-  a.n_zero = L.dtime_part ? DTIME_BINS * p.H * p.nb : 0;
+  // 8 bytes per partial entry (see make_layout): DTIME_BINS histograms for
+  // the bf16 backward, one table for the fp32 one
+  a.n_zero = L.dtime_part ? 2 * (p.dtype == HSTU_BF16 ? DTIME_BINS : 1) * p.H * p.nb : 0;
   return a;
 }
 

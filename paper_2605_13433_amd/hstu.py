@@ -40,7 +40,8 @@ class HstuError(RuntimeError):
 
 class Rab(ctypes.Structure):
     _fields_ = [("pos_w", ctypes.c_void_p), ("time_w", ctypes.c_void_p),
-                ("timestamps", ctypes.c_void_p), ("num_buckets", ctypes.c_int32)]
+                ("timestamps", ctypes.c_void_p), ("num_buckets", ctypes.c_int32),
+                ("alpha", ctypes.c_float)]
 
 
 class FwdOut(ctypes.Structure):
@@ -57,7 +58,8 @@ class BwdIO(ctypes.Structure):
                 ("dq", ctypes.c_void_p), ("dk", ctypes.c_void_p),
                 ("dv", ctypes.c_void_p), ("du", ctypes.c_void_p),
                 ("d_pos_w", ctypes.c_void_p), ("d_time_w", ctypes.c_void_p),
-                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+                ("deterministic", ctypes.c_int32)]
 
 
 class LayerFwdOut(ctypes.Structure):
@@ -150,9 +152,10 @@ def _stream(stream) -> Optional[int]:
     return getattr(stream, "cuda_stream", stream)
 
 
-def make_rab(pos_w=None, time_w=None, timestamps=None, num_buckets=128) -> Rab:
+def make_rab(pos_w=None, time_w=None, timestamps=None, num_buckets=128,
+             alpha=1.0) -> Rab:
     return Rab(_ptr(pos_w), _ptr(time_w), _ptr(timestamps),
-               int(num_buckets) if time_w is not None else 0)
+               int(num_buckets) if time_w is not None else 0, float(alpha))
 
 
 def _check(rc: int):
@@ -284,12 +287,13 @@ class Plan:
     """Outputs + workspace for one problem shape, allocated once and reused."""
 
     def __init__(self, q, seq_offsets, max_len, pos_w=None, time_w=None,
-                 timestamps=None, num_buckets=128, backward=True):
+                 timestamps=None, num_buckets=128, backward=True, alpha=1.0,
+                 deterministic=False):
         T, H, d = q.shape
         dev = q.device
         self.B = seq_offsets.numel() - 1
         self.N, self.H, self.d, self.T = int(max_len), H, d, T
-        self.rab = make_rab(pos_w, time_w, timestamps, num_buckets)
+        self.rab = make_rab(pos_w, time_w, timestamps, num_buckets, alpha)
         self._keep = (pos_w, time_w, timestamps)
         code = _dtype_code(q)
         self.fwd_ws = _workspace(hstu_jagged_attn_workspace_bytes(
@@ -315,7 +319,7 @@ class Plan:
             self.io = BwdIO(code, T, None, _ptr(self.o), _ptr(self.mean), _ptr(self.rstd),
                             _ptr(self.dq), _ptr(self.dk), _ptr(self.dv), _ptr(self.du),
                             _ptr(self.d_pos), _ptr(self.d_time), _ptr(self.bwd_ws),
-                            self.bwd_ws.numel())
+                            self.bwd_ws.numel(), 1 if deterministic else 0)
 
     def status(self, backward=False, stream=None) -> int:
         """The seq_offsets status word (HSTU_SEQ_* bits) of the last forward
@@ -338,15 +342,16 @@ class Plan:
 
 
 def forward(q, k, v, u, seq_offsets, max_len, pos_w=None, time_w=None,
-            timestamps=None, num_buckets=128) -> FwdResult:
+            timestamps=None, num_buckets=128, alpha=1.0) -> FwdResult:
     plan = Plan(q, seq_offsets, max_len, pos_w, time_w, timestamps, num_buckets,
-                backward=False)
+                backward=False, alpha=alpha)
     return plan.forward(q, k, v, u, seq_offsets)
 
 
 def forward_backward(q, k, v, u, seq_offsets, max_len, dy, pos_w=None, time_w=None,
-                     timestamps=None, num_buckets=128):
-    plan = Plan(q, seq_offsets, max_len, pos_w, time_w, timestamps, num_buckets)
+                     timestamps=None, num_buckets=128, alpha=1.0, deterministic=False):
+    plan = Plan(q, seq_offsets, max_len, pos_w, time_w, timestamps, num_buckets,
+                alpha=alpha, deterministic=deterministic)
     f = plan.forward(q, k, v, u, seq_offsets)
     g = plan.backward(q, k, v, u, seq_offsets, dy)
     return f, g

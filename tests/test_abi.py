@@ -157,3 +157,13 @@ def test_layer_workspace_query_rejects_bad_sizes():
     assert "d_model = 100" in hstu.last_error()
     assert lib.hstu_layer_workspace_bytes(2, 64, 2, 64, 128, 10, 0, 1, None) == 0
     assert "HSTU_BF16" in hstu.last_error()
+
+
+def test_alpha_must_be_finite():
+    lib = hstu.load_library()
+    for bad in (float("nan"), float("inf"), -float("inf")):
+        r = hstu.Rab(FAKE, None, None, 0, bad)
+        out = hstu.FwdOut(hstu.HSTU_BF16, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30)
+        rc = lib.hstu_jagged_attn_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 64, 2, 64,
+                                      ctypes.byref(r), ctypes.byref(out), None)
+        assert rc == -1 and "alpha" in hstu.last_error()
