@@ -286,6 +286,52 @@ def embedding_bench(stream, steps, warmup, dtype_name="f32"):
     }
 
 
+def rab_bench(stream, steps, warmup, idx=3):
+    """The standalone RAB operator on workload `idx` (position table, time
+    buckets and the functional time encoding): the jagged bias tensor the
+    fused attention never materialises, its size, and forward / backward
+    times with HIP events on the launch stream (HBM roofline on the bytes
+    of that tensor: written by the forward, read by the backward)."""
+    import torch
+    from paper_2605_13433_amd import hstu, inputs
+    w = inputs.workload(idx)
+    L = w.lengths.astype(np.int64)
+    S = int((L * L).sum())
+    fn = torch.tensor([[0.3, 0.5]] * w.H, dtype=torch.float32)
+    dev = lambda t: None if t is None else t.contiguous().cuda()
+    plan = hstu.RabPlan(dev(w.seq_offsets), w.N, w.H, w.T, S, dev(w.pos_w), dev(w.time_w),
+                        dev(fn), dev(w.timestamps), w.num_buckets)
+    g = torch.randn(w.H, S, device="cuda", dtype=torch.float32)
+
+    def timed(fn_):
+        for _ in range(warmup):
+            fn_()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn_()
+        z.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / steps * 1e3
+
+    fwd_us = timed(lambda: plan.forward(stream))
+    bwd_us = timed(lambda: plan.backward(g, stream))
+    nbytes = 4 * w.H * S
+    gbs = nbytes / (fwd_us * 1e-6) / 1e9
+    return {
+        "workload": w.name, "H": w.H, "square_elements_per_head": S,
+        "materialized_bytes": nbytes,
+        "fwd_us": round(fwd_us, 2), "bwd_us": round(bwd_us, 2),
+        "fwd_GB_s": round(gbs, 1),
+        "bwd_GB_s": round(nbytes / (bwd_us * 1e-6) / 1e9, 1),
+        "roofline": {"bound": "hbm", "kernel": "rab_fwd", "achieved": round(gbs, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "algorithmic_bytes": nbytes},
+    }
+
+
 def cpu_baseline(w, target_s=20.0):
     """The oracle, as it stands, on a bounded sample of the same workload:
     whole sequences in a seeded random order until the estimated
@@ -620,6 +666,8 @@ def main():
                     help="skip the embedding-lookup measurement")
     ap.add_argument("--embedding-only", action="store_true",
                     help="only time the embedding lookup (prints its JSON object)")
+    ap.add_argument("--rab-only", action="store_true",
+                    help="only time the standalone RAB operator (workloads 2-4)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device copies of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
@@ -667,6 +715,10 @@ def main():
     if args.embedding_only:
         for dt in ("f32", "bf16"):
             print(json.dumps(embedding_bench(stream, args.steps, args.warmup, dt)), flush=True)
+        return
+    if args.rab_only:
+        for idx in (2, 3, 4):
+            print(json.dumps(rab_bench(stream, args.steps, args.warmup, idx)), flush=True)
         return
 
     w = inputs.workload(args.workload, args.seed)
@@ -792,6 +844,8 @@ def main():
 
     if not args.no_embedding:
         out["embedding"] = embedding_bench(stream, args.config_steps, min(args.warmup, 5))
+        torch.cuda.empty_cache()
+        out["rab_standalone"] = rab_bench(stream, args.config_steps, min(args.warmup, 5))
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:

@@ -311,6 +311,64 @@ int hstu_profile_enable(int on);
 int hstu_profile_read(int max, const char **names, double *total_ms,
                       int *launches);
 
+/* ---------------------------------------------------------------------
+ * Standalone relative attention bias (RAB) operator.
+ *
+ * The bias of Sec. 4.1.1's operator produced on its own, as the jagged
+ * tensor an unfused attention would add to its scores, with its backward
+ * into the bias parameters (the fused attention above never materialises
+ * it).  For sequence b (L = L_b), head h and local i, j < L:
+ *
+ *   rab[h][sq[b] + i*L + j] = pos_w[h, j - i + N - 1]                (if given)
+ *                           + time_w[h, bucket(ts_i - ts_j)]         (if given)
+ *                           + a_h (1 + |ts_i - ts_j|)^(-beta_h)      (if time_fn)
+ *
+ * sq[b] = sum of L_b'^2 over b' < b (one L x L square per sequence, no
+ * padding; total_square = sq[B]).  bucket() is the rule above.  time_fn
+ * [H][2] = (a_h, beta_h) is a functional time encoding: the paper uses
+ * functional time encodings for FuXi (Appendix A) without a formula; the
+ * library reads them as this per-head power-law decay with learnable
+ * amplitude and exponent.
+ *
+ * Backward, given d_rab in the same layout (all L x L entries count):
+ * d_pos_w[h][x] and d_time_w[h][k] sum d_rab over the entries with that
+ * offset / bucket (unreached entries 0), d_time_fn[h] = (sum d_rab g,
+ * -sum d_rab a_h g ln(1 + |dt|)) with g = (1 + |dt|)^(-beta_h).  All sums
+ * are 64-bit fixed point (resolution 2^-32, |partial sums| < 2^31) added
+ * with integer atomics, so the result is bitwise reproducible.
+ *
+ * Layout: rab and d_rab are float32 [H][total_square].  Tiles are 64 x 64
+ * squares of each sequence's L x L block (the paper's square tiling for
+ * bias tensors).  Contract on seq_offsets as for the attention (clamped
+ * to max_len on the device); the caller sizes rab from sq[B], computed on
+ * the host from its copy of the lengths.
+ * ------------------------------------------------------------------- */
+typedef struct {
+    const float *pos_w;          /* [H][2*max_len-1] or NULL                 */
+    const float *time_w;         /* [H][num_buckets] or NULL                 */
+    const float *time_fn;        /* [H][2] (a_h, beta_h) or NULL             */
+    const int64_t *timestamps;   /* [T]; required iff time_w or time_fn      */
+    int32_t num_buckets;         /* >= 1 iff time_w != NULL                  */
+} hstu_rab_params;
+
+/* Workspace bytes of a standalone RAB call (forward or backward). */
+size_t hstu_jagged_rab_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
+                                       const hstu_rab_params *rp);
+
+/* rab [H][total_square] (float32) from the parameters. */
+int hstu_jagged_rab_fwd(const int64_t *seq_offsets, int32_t B, int32_t max_len,
+                        int32_t H, int64_t total_tokens, int64_t total_square,
+                        const hstu_rab_params *rp, float *rab,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/* Parameter gradients from d_rab [H][total_square]; each output is
+ * overwritten and required iff its parameter is given in rp. */
+int hstu_jagged_rab_bwd(const int64_t *seq_offsets, int32_t B, int32_t max_len,
+                        int32_t H, int64_t total_tokens, int64_t total_square,
+                        const hstu_rab_params *rp, const float *d_rab,
+                        float *d_pos_w, float *d_time_w, float *d_time_fn,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
 /* Thread-local description of the last failure ("" if none). */
 const char *hstu_last_error(void);
 

@@ -62,6 +62,12 @@ class BwdIO(ctypes.Structure):
                 ("deterministic", ctypes.c_int32)]
 
 
+class RabParams(ctypes.Structure):
+    _fields_ = [("pos_w", ctypes.c_void_p), ("time_w", ctypes.c_void_p),
+                ("time_fn", ctypes.c_void_p), ("timestamps", ctypes.c_void_p),
+                ("num_buckets", ctypes.c_int32)]
+
+
 class LayerFwdOut(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int), ("total_tokens", ctypes.c_int64),
                 ("out", ctypes.c_void_p), ("h", ctypes.c_void_p), ("z", ctypes.c_void_p),
@@ -116,6 +122,15 @@ def load_library(path: str = LIB_PATH):
     lib.hstu_layer_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i64, i32,
                                                ctypes.c_int, ctypes.POINTER(Rab)]
     lib.hstu_layer_workspace_bytes.restype = ctypes.c_size_t
+    RP = ctypes.POINTER(RabParams)
+    lib.hstu_jagged_rab_workspace_bytes.argtypes = [i32, i32, i32, RP]
+    lib.hstu_jagged_rab_workspace_bytes.restype = ctypes.c_size_t
+    lib.hstu_jagged_rab_fwd.argtypes = [P, i32, i32, i32, i64, i64, RP, P, P,
+                                        ctypes.c_size_t, P]
+    lib.hstu_jagged_rab_fwd.restype = ctypes.c_int
+    lib.hstu_jagged_rab_bwd.argtypes = [P, i32, i32, i32, i64, i64, RP, P, P, P, P, P,
+                                        ctypes.c_size_t, P]
+    lib.hstu_jagged_rab_bwd.restype = ctypes.c_int
     lib.hstu_jagged_status.argtypes = [P, P, P]
     lib.hstu_jagged_status.restype = ctypes.c_int
     lib.hstu_last_error.argtypes = []
@@ -236,6 +251,66 @@ def hstu_jagged_status(workspace, status, stream=None) -> None:
     """Enqueues the copy of the seq_offsets status word of the last call that
     used `workspace` into `status` (an int32 tensor of one element)."""
     _check(load_library().hstu_jagged_status(_ptr(workspace), _ptr(status), _stream(stream)))
+
+
+def hstu_jagged_rab_workspace_bytes(B, max_len, H, rp: RabParams) -> int:
+    n = load_library().hstu_jagged_rab_workspace_bytes(int(B), int(max_len), int(H),
+                                                        ctypes.byref(rp))
+    if n == 0:
+        raise HstuError(-1, last_error())
+    return n
+
+
+def hstu_jagged_rab_fwd(seq_offsets, B, max_len, H, total_tokens, total_square,
+                        rp: RabParams, rab, workspace, stream=None) -> None:
+    _check(load_library().hstu_jagged_rab_fwd(
+        _ptr(seq_offsets), int(B), int(max_len), int(H), int(total_tokens),
+        int(total_square), ctypes.byref(rp), _ptr(rab), _ptr(workspace), workspace.numel(),
+        _stream(stream)))
+
+
+def hstu_jagged_rab_bwd(seq_offsets, B, max_len, H, total_tokens, total_square,
+                        rp: RabParams, d_rab, d_pos_w, d_time_w, d_time_fn, workspace,
+                        stream=None) -> None:
+    _check(load_library().hstu_jagged_rab_bwd(
+        _ptr(seq_offsets), int(B), int(max_len), int(H), int(total_tokens),
+        int(total_square), ctypes.byref(rp), _ptr(d_rab), _ptr(d_pos_w), _ptr(d_time_w),
+        _ptr(d_time_fn), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+class RabPlan:
+    """Standalone RAB: parameters, workspace and output of one batch; the
+    caller passes the square size (sum of squared lengths) from its host copy
+    of the lengths."""
+
+    def __init__(self, seq_offsets, max_len, H, total_tokens, total_square, pos_w=None,
+                 time_w=None, time_fn=None, timestamps=None, num_buckets=128):
+        self.B = seq_offsets.numel() - 1
+        self.N, self.H, self.T, self.S = int(max_len), int(H), int(total_tokens), \
+            int(total_square)
+        self.rp = RabParams(_ptr(pos_w), _ptr(time_w), _ptr(time_fn), _ptr(timestamps),
+                            int(num_buckets) if time_w is not None else 0)
+        self._keep = (seq_offsets, pos_w, time_w, time_fn, timestamps)
+        dev = seq_offsets.device
+        self.ws = _workspace(hstu_jagged_rab_workspace_bytes(self.B, self.N, self.H, self.rp),
+                             dev)
+        self.rab = torch.empty(self.H, self.S, dtype=torch.float32, device=dev)
+        self.d_pos = (torch.empty(self.H, 2 * self.N - 1, dtype=torch.float32, device=dev)
+                      if pos_w is not None else None)
+        self.d_time = (torch.empty(self.H, num_buckets, dtype=torch.float32, device=dev)
+                       if time_w is not None else None)
+        self.d_fn = (torch.empty(self.H, 2, dtype=torch.float32, device=dev)
+                     if time_fn is not None else None)
+
+    def forward(self, stream=None):
+        hstu_jagged_rab_fwd(self._keep[0], self.B, self.N, self.H, self.T, self.S, self.rp,
+                            self.rab, self.ws, stream)
+        return self.rab
+
+    def backward(self, d_rab, stream=None):
+        hstu_jagged_rab_bwd(self._keep[0], self.B, self.N, self.H, self.T, self.S, self.rp,
+                            d_rab, self.d_pos, self.d_time, self.d_fn, self.ws, stream)
+        return self.d_pos, self.d_time, self.d_fn
 
 
 def max_entries(B: int, max_len: int, total_tokens: int) -> int:
