@@ -18,7 +18,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhstu_jagged.so")
 ARCH = "gfx950"
 SOURCES = ["api.cpp", "sched.hip", "attn_bf16.hip", "attn_f32.hip", "norm.hip",
-           "layer.cpp", "layer_kernels.hip", "noalloc.hip", "embedding.hip", "rab.hip"]
+           "layer.cpp", "layer_kernels.hip", "noalloc.hip", "embedding.hip", "rab.hip",
+           "gemm.hip"]
 HEADERS = ["device.h", "internal.h", "sched_impl.h"]
 
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -183,6 +183,13 @@ hipError_t launch_silu_split(const void *h, void *z, int64_t T, int32_t C,
 // dh [T][4C] = dz planes * silu'(h).
 hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
                               int64_t T, int32_t C, int dev, hipStream_t s);
+// Fused f1 of the layer (csrc/gemm.hip): h [M][N] = x [M][K] . w1 [K][N]
+// (bf16, float32 accumulation) and z = silu(h) split into four [M][N/4]
+// planes, in one hand-written MFMA kernel.  Supported when N is a multiple
+// of 128, N/4 of 8 and K of 64.
+bool gemm_f1_silu_supported(int64_t N, int64_t K);
+hipError_t launch_gemm_f1_silu(const void *x, const void *w1, void *h, void *z, int64_t M,
+                               int32_t N, int32_t K, hipStream_t s);
 // Zero `bytes` (a multiple of 4) of device memory with a kernel.
 // out (bf16, n elements, n % 4 == 0) = sum of `parts` float32 arrays of n
 // elements stored back to back at `part`.

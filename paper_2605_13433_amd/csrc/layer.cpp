@@ -371,16 +371,22 @@ int hstu_layer_fwd(const void *x, const void *w1, const void *w2,
   char *z = (char *)out->z;
   const size_t plane = 2 * (size_t)T * C;
 
-  // h = x . w1
-  if ((rc = gemm(dev, rm(false, false, T, 4 * C, D, D, 4 * C, 4 * C), x, w1,
-                 out->h, ws + L.gemm, s, "gemm_f1")) != HSTU_OK)
-    return rc;
   hipError_t e;
-  {
+  if (gemm_f1_silu_supported(4 * C, D)) {
+    // h = x . w1 and the U, V, Q, K planes silu(h) from one hand-written
+    // kernel (the split is the epilogue's store address)
+    prof::Scope ps("gemm_f1_silu", s);
+    e = launch_gemm_f1_silu(x, w1, out->h, z, T, (int32_t)(4 * C), D, s);
+    if (e != hipSuccess) return hip_fail(e, "f1 launch");
+  } else {
+    // h = x . w1 on hipBLASLt, then the SiLU + split pass
+    if ((rc = gemm(dev, rm(false, false, T, 4 * C, D, D, 4 * C, 4 * C), x, w1,
+                   out->h, ws + L.gemm, s, "gemm_f1")) != HSTU_OK)
+      return rc;
     prof::Scope ps("silu_split", s);
     e = launch_silu_split(out->h, z, T, (int32_t)C, dev, s);
+    if (e != hipSuccess) return hip_fail(e, "silu split launch");
   }
-  if (e != hipSuccess) return hip_fail(e, "silu split launch");
   hstu_fwd_out fo{HSTU_BF16, T, out->y, out->o, out->ln_mean, out->ln_rstd,
                   ws + L.attn, L.attn_bytes};
   rc = hstu_jagged_attn_fwd(z + 2 * plane, z + 3 * plane, z + plane, z,
