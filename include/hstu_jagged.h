@@ -204,9 +204,13 @@ size_t hstu_jagged_attn_workspace_bytes(int32_t B, int32_t max_len, int32_t H,
  *   out = y . w2                       f2 GEMM      [T][d_model]
  *
  * and the backward of sum(out * dout) into dx, dw1, dw2 and the table
- * gradients.  The GEMMs run on hipBLASLt (bf16 in and out, float32
- * accumulation); silu and the split run in one library kernel, its
- * derivative and the merge back in another.  HSTU_BF16 only, d in {64, 128},
+ * gradients.  All products take bf16 in and out with float32 accumulation.
+ * f1 is one hand-written MFMA kernel whose epilogue also writes the planes
+ * silu(h) (when 4*H*d is a multiple of 128 and d_model of 64; otherwise
+ * hipBLASLt and a separate silu + split kernel); the other GEMMs run on
+ * hipBLASLt.  On the way back silu' is applied inside the attention
+ * backward's gradient stores, which write dh [T][4*H*d] directly.
+ * HSTU_BF16 only, d in {64, 128},
  * 1 <= d_model <= 65536 and d_model % 8 == 0.  Weights are row-major:
  * w1 [d_model][4*H*d], w2 [H*d][d_model]; x, out, dx [T][d_model].
  *

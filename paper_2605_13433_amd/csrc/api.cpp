@@ -276,6 +276,70 @@ int attn_fwd_call(const void *q, const void *k, const void *v, const void *u,
   return HSTU_OK;
 }
 
+int attn_bwd_call(const void *q, const void *k, const void *v, const void *u,
+                  const int64_t *seq_offsets, int32_t B, int32_t max_len, int32_t H,
+                  int32_t d, const hstu_rab *rab, hstu_bwd_io *io, void *stream,
+                  const GradOut *go) {
+  if (!io) return fail(HSTU_EINVAL, "io is NULL");
+  Problem p;
+  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, io->dtype,
+                    io->total_tokens, &p);
+  if (rc != HSTU_OK) return rc;
+  if (go && p.dtype != HSTU_BF16)
+    return fail(HSTU_ENOTSUP, "fused gradient outputs need HSTU_BF16");
+  if (p.T > 0 && (!io->dy || !io->o || !io->ln_mean || !io->ln_rstd || !io->dq ||
+                  !io->dk || !io->dv || !io->du))
+    return fail(HSTU_EINVAL, "io->dy, o, ln_mean, ln_rstd, dq, dk, dv, du must be non-null");
+  if (p.has_pos && !io->d_pos_w)
+    return fail(HSTU_EINVAL, "rab->pos_w given but io->d_pos_w is NULL");
+  if (p.has_time && !io->d_time_w)
+    return fail(HSTU_EINVAL, "rab->time_w given but io->d_time_w is NULL");
+  if (p.T == 0 && !p.has_pos && !p.has_time) return HSTU_OK;
+  p.deterministic = io->deterministic != 0;
+  int dev = 0;
+  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
+  Layout L = make_layout(p, true, dev);
+  if ((rc = check_workspace(L, io->workspace, io->workspace_bytes)) != HSTU_OK)
+    return rc;
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a{q, k, v, u,
+             rab ? rab->pos_w : nullptr,
+             p.has_time ? rab->time_w : nullptr,
+             p.has_time ? rab->timestamps : nullptr,
+             io->workspace, L, p};
+  char *ws = (char *)io->workspace;
+  float *d_pos = p.has_pos ? io->d_pos_w : nullptr;
+  float *d_time = p.has_time ? io->d_time_w : nullptr;
+  hipError_t e;
+  if (p.T > 0) {
+    // the LayerNorm backward launch also builds the work lists
+    prof::Scope ps("ln_bwd", s);
+    e = launch_ln_bwd_sched(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
+                            ws + L.dO,
+                            (L.dpos_part && p.dtype == HSTU_BF16) ? ws + L.dpos_part : nullptr,
+                            seq_offsets, ws, L, go, s);
+    if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
+  } else {
+    prof::Scope ps("schedule", s);
+    e = launch_schedule(seq_offsets, p, ws, L, s);
+    if (e != hipSuccess) return hip_fail(e, "schedule launch");
+  }
+  if (p.dtype == HSTU_BF16) {
+    e = launch_attn_bwd_bf16(a, ws + L.dO, io->dq, io->dk, io->dv, go, s);
+    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
+    {
+      prof::Scope ps("finalize_tables", s);
+      e = launch_finalize_tables(a, d_pos, d_time, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "table finalize launch");
+  } else {
+    prof::Scope ps("attn_bwd_f32", s);
+    e = launch_attn_bwd_f32(a, ws + L.dO, io->dq, io->dk, io->dv, d_pos, d_time, s);
+    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
+  }
+  return HSTU_OK;
+}
+
 }  // namespace hstu
 
 using namespace hstu;
@@ -347,62 +411,7 @@ int hstu_jagged_attn_bwd(const void *q, const void *k, const void *v,
                          int32_t max_len, int32_t H, int32_t d,
                          const hstu_rab *rab, hstu_bwd_io *io, void *stream) {
   g_last_error.clear();
-  if (!io) return fail(HSTU_EINVAL, "io is NULL");
-  Problem p;
-  int rc = validate(q, k, v, u, seq_offsets, B, max_len, H, d, rab, io->dtype,
-                    io->total_tokens, &p);
-  if (rc != HSTU_OK) return rc;
-  if (p.T > 0 && (!io->dy || !io->o || !io->ln_mean || !io->ln_rstd || !io->dq ||
-                  !io->dk || !io->dv || !io->du))
-    return fail(HSTU_EINVAL, "io->dy, o, ln_mean, ln_rstd, dq, dk, dv, du must be non-null");
-  if (p.has_pos && !io->d_pos_w)
-    return fail(HSTU_EINVAL, "rab->pos_w given but io->d_pos_w is NULL");
-  if (p.has_time && !io->d_time_w)
-    return fail(HSTU_EINVAL, "rab->time_w given but io->d_time_w is NULL");
-  if (p.T == 0 && !p.has_pos && !p.has_time) return HSTU_OK;
-  p.deterministic = io->deterministic != 0;
-  int dev = 0;
-  if ((rc = current_device(&dev)) != HSTU_OK) return rc;
-  Layout L = make_layout(p, true, dev);
-  if ((rc = check_workspace(L, io->workspace, io->workspace_bytes)) != HSTU_OK)
-    return rc;
-  hipStream_t s = (hipStream_t)stream;
-  AttnArgs a{q, k, v, u,
-             rab ? rab->pos_w : nullptr,
-             p.has_time ? rab->time_w : nullptr,
-             p.has_time ? rab->timestamps : nullptr,
-             io->workspace, L, p};
-  char *ws = (char *)io->workspace;
-  float *d_pos = p.has_pos ? io->d_pos_w : nullptr;
-  float *d_time = p.has_time ? io->d_time_w : nullptr;
-  hipError_t e;
-  if (p.T > 0) {
-    // the LayerNorm backward launch also builds the work lists
-    prof::Scope ps("ln_bwd", s);
-    e = launch_ln_bwd_sched(p, io->dy, u, io->o, io->ln_mean, io->ln_rstd, io->du,
-                            ws + L.dO,
-                            (L.dpos_part && p.dtype == HSTU_BF16) ? ws + L.dpos_part : nullptr,
-                            seq_offsets, ws, L, s);
-    if (e != hipSuccess) return hip_fail(e, "layernorm backward launch");
-  } else {
-    prof::Scope ps("schedule", s);
-    e = launch_schedule(seq_offsets, p, ws, L, s);
-    if (e != hipSuccess) return hip_fail(e, "schedule launch");
-  }
-  if (p.dtype == HSTU_BF16) {
-    e = launch_attn_bwd_bf16(a, ws + L.dO, io->dq, io->dk, io->dv, s);
-    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
-    {
-      prof::Scope ps("finalize_tables", s);
-      e = launch_finalize_tables(a, d_pos, d_time, s);
-    }
-    if (e != hipSuccess) return hip_fail(e, "table finalize launch");
-  } else {
-    prof::Scope ps("attn_bwd_f32", s);
-    e = launch_attn_bwd_f32(a, ws + L.dO, io->dq, io->dk, io->dv, d_pos, d_time, s);
-    if (e != hipSuccess) return hip_fail(e, "attention backward launch");
-  }
-  return HSTU_OK;
+  return attn_bwd_call(q, k, v, u, seq_offsets, B, max_len, H, d, rab, io, stream, nullptr);
 }
 
 int hstu_jagged_status(const void *workspace, int32_t *status, void *stream) {

@@ -77,6 +77,10 @@ struct KParams {
   const WorkEntry *list;
   u16 *out0, *out1;
   u16 *dq_out;
+  // backward outputs: row stride (elements), and with h_* set, each stored
+  // gradient multiplied by silu' of h_* at the same index
+  const u16 *h_dq, *h_dk, *h_dv;
+  int32_t out_stride;
   void *dpos_part, *dtime_part;        // float, or fixed point (deterministic)
   int32_t H, N, nb;
   float inv_n;
@@ -221,26 +225,43 @@ __device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, i
   return dyn;
 }
 
+// Chunks of a 64 x D bf16 tile per thread: chunk tid + THREADS x (x < this)
+// is row ch / (D/8), columns 8 (ch % (D/8)) .. +7.
+template <int D> constexpr int TILE_CHUNKS = TILE * D / 8 / THREADS;
+
 // Coalesced bf16 store of a 64 x D fp32 tile in LDS: every thread converts 8
 // consecutive floats of one row, scales them by `scale` and writes them as a
-// single 16-byte chunk; rows at or beyond `valid` are not written.
+// single 16-byte chunk; rows at or beyond `valid` are not written.  With
+// `silu` set, each value is also multiplied by silu'(h) for the bf16 h of
+// the same chunk in `hv` (a SiLU's backward fused into the store; the
+// caller loads hv early so that its latency is hidden).
 template <int D>
 __device__ __forceinline__ void store_rows(const float *red, int tid, u16 *__restrict__ out,
-                                           int row_stride, int valid, float scale) {
-  constexpr int CH = TILE * D / 8 / THREADS;
+                                           int row_stride, int valid, float scale, bool silu,
+                                           const uint4 (&hv)[TILE_CHUNKS<D>]) {
 #pragma unroll
-  for (int x = 0; x < CH; ++x) {
+  for (int x = 0; x < TILE_CHUNKS<D>; ++x) {
     const int ch = tid + THREADS * x;
     const int row = ch / (D / 8), c8 = ch % (D / 8);
     if (row < valid) {
       const float4 a = *(const float4 *)(red + row * D + 8 * c8);
       const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
+      float f[8] = {scale * a.x, scale * a.y, scale * a.z, scale * a.w,
+                    scale * b.x, scale * b.y, scale * b.z, scale * b.w};
+      if (silu) {
+        const uint32_t hw[4] = {hv[x].x, hv[x].y, hv[x].z, hv[x].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[2 * e] *= dsilu_f(__uint_as_float(hw[e] << 16));
+          f[2 * e + 1] *= dsilu_f(__uint_as_float(hw[e] & 0xffff0000u));
+        }
+      }
       uint4 pk;
-      pk.x = pack2(scale * a.x, scale * a.y);
-      pk.y = pack2(scale * a.z, scale * a.w);
-      pk.z = pack2(scale * b.x, scale * b.y);
-      pk.w = pack2(scale * b.z, scale * b.w);
-      *(uint4 *)(out + row * row_stride + 8 * c8) = pk;
+      pk.x = pack2(f[0], f[1]);
+      pk.y = pack2(f[2], f[3]);
+      pk.z = pack2(f[4], f[5]);
+      pk.w = pack2(f[6], f[7]);
+      *(uint4 *)(out + (int64_t)row * row_stride + 8 * c8) = pk;
     }
   }
 }
@@ -256,7 +277,8 @@ template <int D>
 __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D / 32],
                                                bool writer, int half, int g, int l32,
                                                int tid, u16 *__restrict__ out,
-                                               int row_stride, int valid, float scale) {
+                                               int row_stride, int valid, float scale,
+                                               bool silu, const uint4 (&hv)[TILE_CHUNKS<D>]) {
   lds_barrier();
   if (writer) {
 #pragma unroll
@@ -274,7 +296,7 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
         red[(32 * half + c_row(r, g)) * D + 32 * db + l32] += acc[db][r];
   }
   lds_barrier();
-  store_rows<D>(red, tid, out, row_stride, valid, scale);
+  store_rows<D>(red, tid, out, row_stride, valid, scale, silu, hv);
 }
 
 // Store of a 64 x D fp32 output tile whose 32 x 32 blocks are held by one
@@ -283,13 +305,14 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
 template <int D>
 __device__ __forceinline__ void quad_store_tile(float *red, const f32x16 &acc, int half, int cb,
                                                 int g, int l32, int tid, u16 *__restrict__ out,
-                                                int row_stride, int valid, float scale) {
+                                                int row_stride, int valid, float scale,
+                                                bool silu, const uint4 (&hv)[TILE_CHUNKS<D>]) {
   static_assert(D == 64, "four 32 x 32 blocks");
   lds_barrier();
 #pragma unroll
   for (int r = 0; r < 16; ++r) red[(32 * half + c_row(r, g)) * D + 32 * cb + l32] = acc[r];
   lds_barrier();
-  store_rows<D>(red, tid, out, row_stride, valid, scale);
+  store_rows<D>(red, tid, out, row_stride, valid, scale, silu, hv);
 }
 
 // ------------------------------------------------- swizzled DMA-fed tiles
@@ -593,9 +616,10 @@ attn_fwd_kernel(KParams P) {
     // the popped index goes out through the epilogue's barriers; sum the
     // two key halves in the last tile's buffer, store O (bf16)
     if (tid == 0) sm.next[item_no & 1] = nxt2;
+    const uint4 no_h[TILE_CHUNKS<D>] = {};
     sum_store_tile<D>((float *)sm.tile[(phase - 1) & 1], oacc, wj == 0, wi, g, l32, tid,
                       P.out0 + ((it.start + (int64_t)qt * TILE) * P.H + h) * D,
-                      row_stride, q_valid, 1.0f);
+                      row_stride, q_valid, 1.0f, false, no_h);
     if (!has_next) break;
     cur = nxt;
     it = nit;
@@ -616,7 +640,7 @@ attn_fwd_kernel(KParams P) {
 // keys/queries contribute exact zeros to every product.
 template <int D>
 struct TileRegs {
-  static constexpr int CPT = TILE * D / 8 / THREADS;   // chunks per thread
+  static constexpr int CPT = TILE_CHUNKS<D>;   // chunks per thread
   uint4 c[CPT];
 
   __device__ __forceinline__ void load(const u16 *__restrict__ tile_base,
@@ -710,14 +734,9 @@ struct TimeRun {
 };
 
 
-// silu'(x) = sigma(x) (1 + x (1 - sigma(x))).  The backward kernels work
-// with N dS and N A (the 1/N of both is applied once, to the accumulated
-// dQ, dK, dV tiles at their store and to the table gradients when they are
-// finalized).
-__device__ __forceinline__ float dsilu(float x) {
-  const float sg = sigmoid_f(x);
-  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f);
-}
+// The backward kernels work with N dS and N A (the 1/N of both is applied
+// once, to the accumulated dQ, dK, dV tiles at their store and to the table
+// gradients when they are finalized).
 
 // Table-gradient accumulation types: LDS sums in double and global partials
 // in float, or (deterministic mode) both as 64-bit fixed point, whose
@@ -781,6 +800,8 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     const int q_valid = si.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
     const int64_t qoff = ((si.start + (int64_t)qt * TILE) * P.H + h) * D;
+    const int64_t ooff = (si.start + (int64_t)qt * TILE) * P.out_stride + h * D;
+    const bool fuse = P.h_dq != nullptr;
 
     // every load of the item's start is issued before any of them is used,
     // so the start costs one memory latency; timestamps of rows past the
@@ -836,7 +857,13 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
-      if (kt == qt) pop_next(P, tid, nxt);
+      if (kt == qt) {
+        pop_next(P, tid, nxt);
+        // K, V registers are free from here: they take the h chunks of the
+        // fused silu' store (d=64; at d=128 they are loaded after the loop,
+        // which keeps them out of the loop's register peak)
+        if (D == 64 && fuse) kr.load(P.h_dq + ooff, q_valid, P.out_stride, tid);
+      }
       if (kt < qt) {
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
@@ -918,8 +945,9 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       }
     }
 
-    sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + qoff,
-                      row_stride, q_valid, P.dqk_scale);
+    if (D != 64 && fuse) kr.load(P.h_dq + ooff, q_valid, P.out_stride, tid);
+    sum_store_tile<D>(&sm.red[0][0], acc, wj == 0, wi, g, l32, tid, P.dq_out + ooff,
+                      P.out_stride, q_valid, P.dqk_scale, fuse, kr.c);
 }
 
 // ------------------------------------------------------------------ dK/dV
@@ -939,7 +967,7 @@ struct DkvSmem {
   typename TabAcc<DET>::L pwin[POS ? 2 : 1][POS ? 2 : 1][POS ? 2 * TILE : 1];   // [window][g][slot]
   // At d=64 the item's stationary K and V tiles live here (swizzled, filled
   // by global-to-LDS loads) instead of in registers, which lets the kernel
-  // run three waves per SIMD.
+  // run three waves per SIMD without the time bias (two with it).
   alignas(16) u16 kst[D == 64 ? TILE * D : 8];
   alignas(16) u16 vst[D == 64 ? TILE * D : 8];
 };
@@ -986,7 +1014,7 @@ __device__ __forceinline__ f32x16 dq0_block(const u16 *dsb, const u16 *kst, int 
 // One k-stationary item: dV_j, dK_j for a 64-row key tile of one head over
 // its query tiles, with the table gradients (d_pos through the sheared tile
 // and the rolling diagonal window, d_time through per-lane index runs).
-template <int D, bool POS, bool TIME, bool DET>
+template <int D, bool POS, bool TIME, bool DET, bool KV_LDS>
 __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> &smx,
                                          float *dyn, typename TabAcc<DET>::L *tacc,
                                          const int tid0, const WorkEntry e, const int h,
@@ -1009,12 +1037,13 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     const int k_valid = si.len - kt * TILE;
     const int j_loc = 32 * wj + l32;
     const int64_t koff = ((si.start + (int64_t)kt * TILE) * P.H + h) * D;
+    const int64_t ooff = (si.start + (int64_t)kt * TILE) * P.out_stride + h * D;
+    const bool fuse = P.h_dk != nullptr;
 
     // stationary K, V rows: registers, or (d=64) LDS tiles whose rows past
     // the sequence repeat its last row -- those keys only occur in the last
     // key tile's diagonal step, where the causal mask removes them, and
     // query rows past the sequence carry dO = 0
-    constexpr bool KV_LDS = D == 64;
     // dQ of a sequence's first q-tile comes from its tile pair (0, 0) alone:
     // with `dsb` given, the item of k-tile 0 stages that pair's dS^T in
     // `dsb` ([key][query], stride DS_STRIDE) and computes dQ = dS K against
@@ -1033,6 +1062,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     // (one memory latency); timestamps of rows past the sequence repeat its
     // last row (those rows are always masked)
     TileRegs<D> qr, dr;
+    TileRegs<D> hq;                       // h chunks of the first tile's dQ (fused store)
     const int64_t r0k = si.start + (int64_t)kt * TILE;
     qr.load(P.q + (r0k * P.H + h) * D, k_valid, row_stride, tid);
     dr.load(P.dO + (r0k * P.H + h) * D, k_valid, row_stride, tid);
@@ -1093,7 +1123,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       lds_barrier();
       const bool slow = TIME && sm.flag[phase & 1] != 0;
       if (TIME && tid == 0) sm.flag[(phase + 1) & 1] = 0;
-      if (qt + 1 == si.ntiles) pop_next(P, tid, nxt);
+      if (qt + 1 == si.ntiles) {
+        pop_next(P, tid, nxt);
+        // Q, dO registers are free from here: they take the h chunks of
+        // the fused silu' stores
+        if (fuse) {
+          qr.load(P.h_dk + ooff, k_valid, P.out_stride, tid);
+          dr.load(P.h_dv + ooff, k_valid, P.out_stride, tid);
+          if (with_dq) hq.load(P.h_dq + ooff, k_valid, P.out_stride, tid);
+        }
+      }
       if (qt + 1 < si.ntiles) {
         const int nv = si.len - (qt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
@@ -1244,12 +1283,13 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     if constexpr (KV_LDS) {
       if (with_dq)
         quad_store_tile<D>(&sm.red[0][0], dq0_block<D>(dsb, smx.kst, wi, wj, g, lane), wi, wj,
-                           g, l32, tid, P.dq_out + koff, row_stride, k_valid, P.dqk_scale);
+                           g, l32, tid, P.dq_out + ooff, P.out_stride, k_valid, P.dqk_scale,
+                           fuse, hq.c);
     }
-    sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + koff,
-                      row_stride, k_valid, P.dqk_scale);
-    sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + koff,
-                      row_stride, k_valid, P.inv_n);
+    sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + ooff,
+                      P.out_stride, k_valid, P.dqk_scale, fuse, qr.c);
+    sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + ooff,
+                      P.out_stride, k_valid, P.inv_n, fuse, dr.c);
 }
 
 // Work-group start of the kernels that run dK/dV items: zeroed d_time
@@ -1316,8 +1356,8 @@ attn_bwd_kernel(KParams P) {
       e.tile &= ~BWD_DQ_FLAG;
       dq_item<D, POS, TIME>(P, sm, dyn, tid0, e, h, phase, nxt);
     } else {
-      dkv_item<D, POS, TIME, DET>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v, nxt,
-                                  P.fuse_dq0 ? dsb : nullptr);
+      dkv_item<D, POS, TIME, DET, D == 64>(P, smx, dyn, tacc, tid0, e, h, phase, pend_p, pend_v,
+                                           nxt, P.fuse_dq0 ? dsb : nullptr);
     }
   }
   dkv_kernel_fini<D, POS, TIME, DET>(P, tacc, tid0, pend_p, pend_v);
@@ -1359,8 +1399,10 @@ attn_bwd_dkv_kernel(KParams P) {
   typename A::G pend_v = 0;
   int nxt = 0;
   for (int item = blockIdx.x; item < n_items; item = take_next(&sm.item, tid0, nxt))
-    dkv_item<D, POS, TIME, DET>(P, smx, dyn, tacc, tid0, P.list[item / P.H], item % P.H,
-                                phase, pend_p, pend_v, nxt);
+    // K, V stationary in LDS at d=64 (in registers the kernel measured
+    // 5-10% slower on the Zipf batch of 1024 sequences)
+    dkv_item<D, POS, TIME, DET, D == 64>(P, smx, dyn, tacc, tid0, P.list[item / P.H],
+                                         item % P.H, phase, pend_p, pend_v, nxt);
   dkv_kernel_fini<D, POS, TIME, DET>(P, tacc, tid0, pend_p, pend_v);
 }
 
@@ -1413,6 +1455,7 @@ KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
   P.neg_al2e = -a.p.alpha * L2E;
   P.dqk_scale = a.p.alpha / (float)a.p.N;
   P.all_heads = all_heads(a.p) ? 1 : 0;
+  P.out_stride = a.p.H * a.p.d;
   return P;
 }
 
@@ -1512,17 +1555,26 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
 }
 
 hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
-                                void *dv, hipStream_t s) {
+                                void *dv, const GradOut *go, hipStream_t s) {
   const char *ws = (const char *)a.ws;
   const Problem &p = a.p;
-  if (a.L.bwd_combined) {
-    prof::Scope ps("attn_bwd", s);
-    KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_BWD,
-                            (const WorkEntry *)(ws + a.L.list_b));
+  auto outputs = [&](KParams &P) {
     P.dO = (const u16 *)dO;
     P.out0 = (u16 *)dk;
     P.out1 = (u16 *)dv;
     P.dq_out = (u16 *)dq;
+    if (go) {
+      P.out_stride = go->stride;
+      P.h_dq = (const u16 *)go->h_dq;
+      P.h_dk = (const u16 *)go->h_dk;
+      P.h_dv = (const u16 *)go->h_dv;
+    }
+  };
+  if (a.L.bwd_combined) {
+    prof::Scope ps("attn_bwd", s);
+    KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_BWD,
+                            (const WorkEntry *)(ws + a.L.list_b));
+    outputs(P);
     P.dpos_part = a.L.dpos_part ? (void *)(ws + a.L.dpos_part) : nullptr;
     P.dtime_part = a.L.dtime_part ? (void *)(ws + a.L.dtime_part) : nullptr;
     // must match the scheduler's choice (sched_args)
@@ -1536,9 +1588,7 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
     prof::Scope ps("attn_bwd_dkv", s);
     KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DKV,
                             (const WorkEntry *)(ws + a.L.list_k));
-    P.dO = (const u16 *)dO;
-    P.out0 = (u16 *)dk;
-    P.out1 = (u16 *)dv;
+    outputs(P);
     P.dpos_part = a.L.dpos_part ? (void *)(ws + a.L.dpos_part) : nullptr;
     P.dtime_part = a.L.dtime_part ? (void *)(ws + a.L.dtime_part) : nullptr;
     HSTU_DISPATCH_TAB(attn_bwd_dkv_kernel, p.d, p.has_pos, p.has_time, p.deterministic,
@@ -1550,8 +1600,7 @@ hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, voi
   prof::Scope ps("attn_bwd_dq", s);
   KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_DQ,
                           (const WorkEntry *)(ws + a.L.list_q));
-  P.dO = (const u16 *)dO;
-  P.dq_out = (u16 *)dq;
+  outputs(P);
   HSTU_DISPATCH(attn_bwd_dq_kernel, p.d, p.has_pos, p.has_time,
                 hipLaunchKernelGGL(kfn, dim3(a.L.bwd_grid_dq), dim3(THREADS), q_dyn_bytes(p),
                                    s, P));

@@ -1,6 +1,6 @@
 // Device-side helpers shared by the gfx950 kernels of the jagged HSTU
 // attention library: MFMA operand types, bf16 packing, the relative-time
-// bucket rule and SiLU.
+// bucket rule, SiLU and its derivative.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -91,6 +91,14 @@ __device__ __forceinline__ void lds_barrier() {
 // 2^(+large) = inf gives 0, 2^(-large) = 0 gives 1.
 __device__ __forceinline__ float sigmoid_f(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -1.44269504088896341f));
+}
+
+// silu(x) = x sigma(x) and its derivative silu'(x) = sigma(x) (1 + x (1 -
+// sigma(x))).
+__device__ __forceinline__ float silu_f(float x) { return x * sigmoid_f(x); }
+__device__ __forceinline__ float dsilu_f(float x) {
+  const float sg = sigmoid_f(x);
+  return sg * __builtin_fmaf(x, 1.0f - sg, 1.0f);
 }
 
 }  // namespace hstu

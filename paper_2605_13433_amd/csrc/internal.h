@@ -138,6 +138,23 @@ int attn_fwd_call(const void *q, const void *k, const void *v, const void *u,
                   const FixedScratch *fixed);
 
 
+// Form of the bf16 backward's dq, dk, dv, du outputs: rows of `stride`
+// elements, and with h_* set, each gradient multiplied by silu' of the h_*
+// element at the same index before its store (the HSTU layer writes
+// dh = dz silu'(h) straight into its [T][4C] gradient this way).  Without a
+// GradOut the outputs are plain [T][H*d].
+struct GradOut {
+  int32_t stride;
+  const void *h_dq, *h_dk, *h_dv, *h_du;
+};
+
+// The attention backward (LayerNorm backward with the schedule, attention
+// backward, table finalize); `go` (bf16 only) sets the outputs' form.
+int attn_bwd_call(const void *q, const void *k, const void *v, const void *u,
+                  const int64_t *seq_offsets, int32_t B, int32_t max_len, int32_t H,
+                  int32_t d, const hstu_rab *rab, hstu_bwd_io *io, void *stream,
+                  const GradOut *go);
+
 // ---- launchers (each returns hipSuccess or the launch error) ----
 // Builds the work lists (and zeroes the d_time bins when the layout has
 // them, so the backward's later kernels can accumulate into them).
@@ -157,7 +174,7 @@ hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s);
 // dQ, dK, dV and the table-gradient partials: one combined launch, or a
 // dK/dV launch then a dQ launch (see Layout::bwd_combined).
 hipError_t launch_attn_bwd_bf16(const AttnArgs &a, const void *dO, void *dq, void *dk,
-                                void *dv, hipStream_t s);
+                                void *dv, const GradOut *go, hipStream_t s);
 
 hipError_t launch_attn_fwd_f32(const AttnArgs &a, void *o, hipStream_t s);
 hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
@@ -172,7 +189,7 @@ hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
                                const void *o, const float *mean, const float *rstd,
                                void *du, void *dO, void *dpos_part,
                                const int64_t *seq_offsets, void *ws, const Layout &L,
-                               hipStream_t s);
+                               const GradOut *go, hipStream_t s);
 hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                                   float *d_time, hipStream_t s);
 
@@ -180,9 +197,6 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
 // z planes [4][T][C] = silu(h [T][4C]) split by column blocks.
 hipError_t launch_silu_split(const void *h, void *z, int64_t T, int32_t C,
                              int dev, hipStream_t s);
-// dh [T][4C] = dz planes * silu'(h).
-hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
-                              int64_t T, int32_t C, int dev, hipStream_t s);
 // Fused f1 of the layer (csrc/gemm.hip): h [M][N] = x [M][K] . w1 [K][N]
 // (bf16, float32 accumulation) and z = silu(h) split into four [M][N/4]
 // planes, in one hand-written MFMA kernel.  Supported when N is a multiple

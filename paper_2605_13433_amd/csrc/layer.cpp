@@ -280,7 +280,7 @@ int gemm_wgrad(int dev, int64_t M, int64_t N, int64_t T, const void *A, int64_t 
 }
 
 struct LayerLayout {
-  size_t attn, gemm, dy, dz, dh, part, total;
+  size_t attn, gemm, dy, dh, part, total;
   size_t attn_bytes;
 };
 
@@ -298,7 +298,6 @@ LayerLayout layer_layout(const Problem &p, int64_t D, bool for_bwd, int dev) {
   L.gemm = take(GEMM_WS_BYTES);
   if (for_bwd) {
     L.dy = take(2 * (size_t)p.T * C);
-    L.dz = take(2 * 4 * (size_t)p.T * C);
     L.dh = take(2 * 4 * (size_t)p.T * C);
     // dW2 [C][D] and dW1 [D][4C] run one after the other: one partial area
     L.part = take(std::max(splitk_bytes(C, D, p.T), splitk_bytes(D, 4 * C, p.T)));
@@ -425,7 +424,8 @@ int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
   char *ws = (char *)io->workspace;
   const int64_t C = (int64_t)H * d, D = d_model;
   const char *z = (const char *)io->z;
-  char *dz = ws + L.dz;
+  const uint16_t *h = (const uint16_t *)io->h;
+  uint16_t *dh = (uint16_t *)(ws + L.dh);   // bf16 elements
   const size_t plane = 2 * (size_t)T * C;
   hipError_t e;
 
@@ -443,19 +443,17 @@ int hstu_layer_bwd(const void *x, const void *w1, const void *w2,
                          (float *)(ws + L.part), ws + L.gemm, s, "gemm_dw2")) != HSTU_OK)
       return rc;
   }
-  // Attention backward into the dz planes (du, dv, dq, dk); also writes the
-  // table gradients (zeros when T = 0).
+  // Attention backward straight into dh [T][4C]: every gradient of the
+  // U, V, Q, K planes is multiplied by silu'(h) at its store, so the planes
+  // dz are never written.  Also writes the table gradients (zeros when
+  // T = 0).
   hstu_bwd_io bo{HSTU_BF16, T, ws + L.dy, io->o, io->ln_mean, io->ln_rstd,
-                 dz + 2 * plane, dz + 3 * plane, dz + plane, dz,
+                 dh + 2 * C, dh + 3 * C, dh + C, dh,
                  io->d_pos_w, io->d_time_w, ws + L.attn, L.attn_bytes};
-  rc = hstu_jagged_attn_bwd(z + 2 * plane, z + 3 * plane, z + plane, z,
-                            seq_offsets, B, max_len, H, d, rab, &bo, stream);
+  const GradOut go{(int32_t)(4 * C), h + 2 * C, h + 3 * C, h + C, h};
+  rc = attn_bwd_call(z + 2 * plane, z + 3 * plane, z + plane, z, seq_offsets, B, max_len, H,
+                     d, rab, &bo, stream, &go);
   if (rc != HSTU_OK || T == 0) return rc;
-  {
-    prof::Scope ps("dsilu_merge", s);
-    e = launch_dsilu_merge(io->h, dz, ws + L.dh, T, (int32_t)C, dev, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "silu backward launch");
   // dx = dh . w1^T ;  dw1 = x^T . dh
   if ((rc = gemm(dev, rm(false, true, T, D, 4 * C, 4 * C, 4 * C, D), ws + L.dh,
                  w1, io->dx, ws + L.gemm, s, "gemm_dx")) != HSTU_OK)

@@ -1,9 +1,9 @@
 // Pointwise kernels of the HSTU layer shell: the SiLU + column split that
-// turns f1's output into the attention's U, V, Q, K planes, its derivative
-// + merge on the way back, the sum of split-K partial products, and a zero
-// fill.
+// turns f1's output into the attention's U, V, Q, K planes (for f1 shapes
+// the fused GEMM does not tile), the sum of split-K partial products, and a
+// zero fill.
 //
-// Both main kernels are pure streaming passes (HBM-bound): each thread moves
+// The split is a pure streaming pass (HBM-bound): each thread moves
 // 16-byte chunks of eight bf16, a chunk never straddles two planes (the
 // plane width H*d is a multiple of 64), and consecutive threads touch
 // consecutive chunks of both the [T][4C] matrix and a plane row, so loads
@@ -18,14 +18,6 @@ namespace hstu {
 namespace {
 
 constexpr int PW_THREADS = 256;
-
-__device__ __forceinline__ float silu_f(float x) { return x * sigmoid_f(x); }
-
-// silu'(x) = s + x s (1 - s), s = sigmoid(x)
-__device__ __forceinline__ float dsilu_f(float x) {
-  const float s = sigmoid_f(x);
-  return s + x * s * (1.0f - s);
-}
 
 __device__ __forceinline__ void unpack8(uint4 v, float f[8]) {
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -63,27 +55,6 @@ silu_split_kernel(const uint4 *__restrict__ h, uint4 *__restrict__ z,
 #pragma unroll
     for (int i = 0; i < 8; ++i) f[i] = silu_f(f[i]);
     z[p * plane_stride_chunks + t * plane_chunks + c] = pack8(f);
-  }
-}
-
-// dh[t][p*C + c] = dz[p][t][c] * silu'(h[t][p*C + c]).
-__global__ void __launch_bounds__(PW_THREADS)
-dsilu_merge_kernel(const uint4 *__restrict__ h, const uint4 *__restrict__ dz,
-                   uint4 *__restrict__ dh, int64_t chunks, int32_t row_chunks,
-                   int32_t plane_chunks, int64_t plane_stride_chunks) {
-  const int64_t stride = (int64_t)gridDim.x * PW_THREADS;
-  for (int64_t x = (int64_t)blockIdx.x * PW_THREADS + threadIdx.x; x < chunks;
-       x += stride) {
-    const int64_t t = x / row_chunks;
-    const int32_t cc = (int32_t)(x - t * row_chunks);
-    const int32_t p = cc / plane_chunks;
-    const int32_t c = cc - p * plane_chunks;
-    float fh[8], fd[8];
-    unpack8(h[x], fh);
-    unpack8(dz[p * plane_stride_chunks + t * plane_chunks + c], fd);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) fd[i] *= dsilu_f(fh[i]);
-    dh[x] = pack8(fd);
   }
 }
 
@@ -127,17 +98,6 @@ hipError_t launch_silu_split(const void *h, void *z, int64_t T, int32_t C,
   hipLaunchKernelGGL(silu_split_kernel, dim3(pw_grid(chunks, dev)),
                      dim3(PW_THREADS), 0, s, (const uint4 *)h, (uint4 *)z,
                      chunks, 4 * C / 8, C / 8, T * (int64_t)C / 8);
-  return hipGetLastError();
-}
-
-hipError_t launch_dsilu_merge(const void *h, const void *dz, void *dh,
-                              int64_t T, int32_t C, int dev, hipStream_t s) {
-  const int64_t chunks = T * 4 * (int64_t)C / 8;
-  if (chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(dsilu_merge_kernel, dim3(pw_grid(chunks, dev)),
-                     dim3(PW_THREADS), 0, s, (const uint4 *)h,
-                     (const uint4 *)dz, (uint4 *)dh, chunks, 4 * C / 8, C / 8,
-                     T * (int64_t)C / 8);
   return hipGetLastError();
 }
 

@@ -109,6 +109,15 @@ ln_fwd_group_kernel(const T *__restrict__ o, const T *__restrict__ u,
   }
 }
 
+// g[e] *= silu'(h[e]) for eight consecutive elements.
+template <typename T>
+__device__ __forceinline__ void silu_back8(const T *__restrict__ h, float g[8]) {
+  float hh[8];
+  Vec8<T>::load(h, hh);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) g[e] *= dsilu_f(hh[e]);
+}
+
 template <typename T, int L>
 __device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *__restrict__ u,
                                              const T *__restrict__ o,
@@ -116,7 +125,8 @@ __device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *
                                              const float *__restrict__ rstd,
                                              T *__restrict__ du, T *__restrict__ dO,
                                              uint64_t *__restrict__ dpos_part, int H,
-                                             int64_t T_tokens, int block) {
+                                             int64_t T_tokens, int block, int64_t du_stride,
+                                             const T *__restrict__ du_h) {
   constexpr int F = 8 * L, TPW = 64 / L;
   const int lane = threadIdx.x & 63, sub = lane % L;
   const int64_t r = ((int64_t)block * LN_WAVES + (threadIdx.x >> 6)) * TPW + lane / L;
@@ -144,7 +154,9 @@ __device__ __forceinline__ void ln_bwd_group(const T *__restrict__ dy, const T *
     o_du[e] = n * g[e];
     o_do[e] = rs * (g[e] * uu[e] - mg - n * mgn);
   }
-  Vec8<T>::store(du + at, o_du);
+  const int64_t du_at = r * du_stride + 8 * sub;
+  if (du_h) silu_back8(du_h + du_at, o_du);
+  Vec8<T>::store(du + du_at, o_du);
   Vec8<T>::store(dO + at, o_do);
   // the attention backward accumulates this token's d_pos partials (8
   // bytes each: a float, or 64-bit fixed point in the deterministic mode)
@@ -199,7 +211,8 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
               const T *__restrict__ o, const float *__restrict__ mean,
               const float *__restrict__ rstd, T *__restrict__ du,
               T *__restrict__ dO, uint64_t *__restrict__ dpos_part, int H,
-              int64_t T_tokens, int F, SchedArgs sa, int sched) {
+              int64_t T_tokens, int F, SchedArgs sa, int sched, int64_t du_stride,
+              const T *__restrict__ du_h) {
   if (sched && blockIdx.x == 0) {
     __shared__ SchedSmem ssm;
     build_schedule<LN_THREADS>(sa, ssm, threadIdx.x);
@@ -210,7 +223,7 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 #define HSTU_LN_GROUP(LL)                                                               \
   case 8 * LL:                                                                          \
     ln_bwd_group<T, LL>(dy, u, o, mean, rstd, du, dO, dpos_part, H, T_tokens,            \
-                        (int)blockIdx.x - sched);                                       \
+                        (int)blockIdx.x - sched, du_stride, du_h);                      \
     return;
     HSTU_LN_GROUP(1) HSTU_LN_GROUP(2) HSTU_LN_GROUP(4) HSTU_LN_GROUP(8)
     HSTU_LN_GROUP(16) HSTU_LN_GROUP(32) HSTU_LN_GROUP(64)
@@ -250,7 +263,8 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
       o_du[e] = n * g[e];
       o_do[e] = rs * (g[e] * uu[e] - mg - n * mgn);
     }
-    Vec8<T>::store(du + base + f0, o_du);
+    if (du_h) silu_back8(du_h + r * du_stride + f0, o_du);
+    Vec8<T>::store(du + r * du_stride + f0, o_du);
     Vec8<T>::store(dO + base + f0, o_do);
   }
   // the attention backward accumulates this token's d_pos partials
@@ -393,7 +407,7 @@ hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
                                const void *o, const float *mean, const float *rstd,
                                void *du, void *dO, void *dpos_part_v,
                                const int64_t *seq_offsets, void *ws, const Layout &L,
-                               hipStream_t s) {
+                               const GradOut *go, hipStream_t s) {
   uint64_t *dpos_part = (uint64_t *)dpos_part_v;
   const int F = p.H * p.d;
   const SchedArgs sa = sched_args(seq_offsets, p, ws, L);
@@ -402,11 +416,13 @@ hipError_t launch_ln_bwd_sched(const Problem &p, const void *dy, const void *u,
   if (p.dtype == HSTU_BF16)
     hipLaunchKernelGGL(ln_bwd_kernel<u16>, grid, dim3(LN_THREADS), 0, s,
                        (const u16 *)dy, (const u16 *)u, (const u16 *)o, mean, rstd,
-                       (u16 *)du, (u16 *)dO, dpos_part, p.H, p.T, F, sa, 1);
+                       (u16 *)du, (u16 *)dO, dpos_part, p.H, p.T, F, sa, 1,
+                       go ? go->stride : (int64_t)F, go ? (const u16 *)go->h_du : nullptr);
   else
     hipLaunchKernelGGL(ln_bwd_kernel<float>, grid, dim3(LN_THREADS), 0, s,
                        (const float *)dy, (const float *)u, (const float *)o, mean, rstd,
-                       (float *)du, (float *)dO, dpos_part, p.H, p.T, F, sa, 1);
+                       (float *)du, (float *)dO, dpos_part, p.H, p.T, F, sa, 1, (int64_t)F,
+                       (const float *)nullptr);
   return hipGetLastError();
 }
 
