@@ -58,7 +58,11 @@ namespace {
 constexpr int THREADS = 256;     // 4 waves
 constexpr int RM_PAD = 8;        // backward: row-major LDS stride D+8 bf16
 constexpr int DS_STRIDE = TILE + RM_PAD;   // backward: staged dS^T tile
-constexpr int POS_COPY = 2 * TILE + 4;
+// Stride (floats) of the four shifted copies of a position-bias slice: at
+// least 2*TILE + 3 entries, and 16 (mod 64) so that the 16 lanes of a 16-byte
+// read phase, whose 4-entry windows start at 16 consecutive entries, fall on
+// 16 distinct 4-bank groups of the 64 banks.
+constexpr int POS_COPY = 144;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
 constexpr float L2E = 1.44269504088896341f;      // log2(e)
@@ -317,22 +321,49 @@ __device__ __forceinline__ void quad_store_tile(float *red, const f32x16 &acc, i
 
 // ------------------------------------------------- swizzled DMA-fed tiles
 // A 64-row tile of one head in LDS without padding: 16-byte chunk c of row r
-// sits at chunk position c ^ (r & 7) of that row, so the row-wise reads (32
-// lanes on 32 consecutive rows, one chunk each) and the transpose reads spread
-// over all banks.  Tiles are filled straight from global memory by the gfx950
-// global-to-LDS loads (each lane's 16 bytes land at the instruction's LDS base
-// + 16 * lane), so no registers or LDS-store instructions stage them.
+// sits at chunk position c ^ swz_key<D, K>(r) of that row.  The LDS has 64
+// banks of 4 bytes (one 256-byte line) and serves a 16-byte read in phases of
+// 16 lanes, an 8-byte (or transpose) read in phases of 32 lanes.  The reads:
+//   row reads: 16 lanes on 16 consecutive rows (aligned), one chunk each;
+//   transpose reads: 32 lanes on 4 consecutive rows (aligned) x 4 chunks
+//     (an aligned group of four), and the same 8 rows further.
+// SWZ_CF makes both conflict-free.  D = 64 (two rows per line, half r & 1):
+// the key takes the 8 values over the 8 rows of each half of a 16-row group,
+// and bit 2 of it (which picks the aligned chunk group) differs between rows
+// r and r+2.  D = 128 (one row per line): the key takes 16 values over 16
+// rows, and its chunk group (bits 2-3) differs between the 4 rows of a
+// transpose read.  SWZ_ROWS8 (key r & 7) leaves 2-way conflicts at D = 64
+// (rows r and r+8 of a row read share a bank group) but gives rows 8 and 16
+// apart the same key, so their addresses differ by an immediate offset: the
+// d=64 forward, bound by its vector ALU work, keeps it (the conflict-free key
+// costs it 11 registers and a wave per SIMD, 9% on the Zipf batch).  Tiles
+// are filled straight from global memory by the gfx950 global-to-LDS loads
+// (each lane's 16 bytes land at the instruction's LDS base + 16 * lane, a
+// contiguous write), so no registers or LDS-store instructions stage them.
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int D>
-__device__ __forceinline__ int swz(int r, int c) {
-  return r * D + 8 * (c ^ (r & 7));
+enum SwzKind { SWZ_ROWS8 = 0, SWZ_CF = 1 };
+
+template <int D, int K>
+__device__ __forceinline__ int swz_key(int r) {
+  static_assert(D == 64 || D == 128, "head dim");
+  if (K == SWZ_ROWS8) return r & 7;
+  return D == 64 ? ((((r >> 1) & 1) << 2) | ((r >> 2) & 3))
+                 : (((r & 3) << 2) | ((r >> 2) & 3));
 }
+
+template <int D, int K>
+__device__ __forceinline__ int swz(int r, int c) {
+  return r * D + 8 * (c ^ swz_key<D, K>(r));
+}
+
+// Key of the forward's K/V tiles.
+template <int D> constexpr int FWD_SWZ = D == 64 ? SWZ_ROWS8 : SWZ_CF;
 
 // Issue the loads of a 64 x D tile (rows of `row_stride` elements from
 // `base`) into `lds`; wave w covers 1/4 of it.  Rows at or beyond `valid`
 // (>= 1) repeat row valid-1: finite data that the caller always masks out.
-template <int D>
+template <int D, int K>
 __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid, int row_stride,
                                          u16 *lds, int w, int lane) {
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
@@ -341,7 +372,7 @@ __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid
   for (int x = 0; x < IPW; ++x) {
     const int pos = (w * IPW + x) * 64 + lane;     // chunk position in LDS
     const int r = pos / CPR;
-    const int c = (pos % CPR) ^ (r & 7);
+    const int c = (pos % CPR) ^ swz_key<D, K>(r);
     const int rr = r < valid ? r : valid - 1;
     __builtin_amdgcn_global_load_lds((const void *)(base + rr * row_stride + 8 * c),
                                      (lds_void *)(lds + (w * IPW + x) * 64 * 8), 16, 0, 0);
@@ -352,19 +383,19 @@ __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid
 // included (they count as vector memory operations, not LDS operations).
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
-template <int D>
+template <int D, int K>
 __device__ __forceinline__ bf16x8 sread_rm(const u16 *lds, int row, int col) {
-  return *(const bf16x8 *)(lds + swz<D>(row, col >> 3));
+  return *(const bf16x8 *)(lds + swz<D, K>(row, col >> 3));
 }
 
 // As read_tr, on a swizzled tile.
-template <int D>
+template <int D, int K>
 __device__ __forceinline__ bf16x8 sread_tr(const u16 *lds, int krow, int ncol, int lane) {
   const int c = lane & 15;
   const int row = krow + (c >> 2);
   const int col = ncol + ((lane >> 4) & 1) * 16 + 4 * (c & 3);
-  const u16 *p0 = lds + swz<D>(row, col >> 3) + (col & 7);
-  const u16 *p1 = lds + swz<D>(row + 8, col >> 3) + (col & 7);
+  const u16 *p0 = lds + swz<D, K>(row, col >> 3) + (col & 7);
+  const u16 *p1 = lds + swz<D, K>(row + 8, col >> 3) + (col & 7);
   const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p0);
   const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p1);
   typedef short v8i16 __attribute__((ext_vector_type(8)));
@@ -412,8 +443,8 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
                                                int row_stride, int64_t &ts_start,
                                                int64_t &ts_i, int64_t &ts_k, float &pos_v) {
   const int64_t hb = (it.start * P.H + it.h) * D;
-  dma_tile<D>(P.k + hb, it.len, row_stride, kbuf, w, lane);
-  dma_tile<D>(P.v + hb, it.len, row_stride, vbuf, w, lane);
+  dma_tile<D, FWD_SWZ<D>>(P.k + hb, it.len, row_stride, kbuf, w, lane);
+  dma_tile<D, FWD_SWZ<D>>(P.v + hb, it.len, row_stride, vbuf, w, lane);
   if (TIME) {
     const int q_valid = it.len - it.tile * TILE;
     ts_start = P.ts[it.start];
@@ -527,8 +558,8 @@ attn_fwd_kernel(KParams P) {
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
-        dma_tile<D>(P.k + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][0], w, lane);
-        dma_tile<D>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
+        dma_tile<D, FWD_SWZ<D>>(P.k + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][0], w, lane);
+        dma_tile<D, FWD_SWZ<D>>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, P.inv_alpha);
@@ -557,7 +588,7 @@ attn_fwd_kernel(KParams P) {
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks)
-        s = mfma32(sread_rm<D>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
+        s = mfma32(sread_rm<D, FWD_SWZ<D>>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
       if (last && has_next)    // the query rows are free: fetch the next item's
         load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
                            i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
@@ -608,7 +639,7 @@ attn_fwd_kernel(KParams P) {
         const bf16x8 pa = as_bf16x8(pk);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(pa, sread_tr<D>(vt_lds, 32 * wj + 16 * hh + 4 * g, 32 * db, lane),
+          oacc[db] = mfma32(pa, sread_tr<D, FWD_SWZ<D>>(vt_lds, 32 * wj + 16 * hh + 4 * g, 32 * db, lane),
                             oacc[db]);
       }
     }
@@ -643,22 +674,18 @@ struct TileRegs {
   static constexpr int CPT = TILE_CHUNKS<D>;   // chunks per thread
   uint4 c[CPT];
 
+  // Rows at or beyond `valid` read as zeros: the loads go through a buffer
+  // resource that ends after row valid-1, so the per-thread offsets are the
+  // same for every tile of a given row stride (one register per chunk).
   __device__ __forceinline__ void load(const u16 *__restrict__ tile_base,
                                        int valid, int row_stride, int tid) {
-    if (valid >= TILE) {
+    const int rows = valid < TILE ? (valid > 0 ? valid : 0) : TILE;
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(tile_base, 2u * (uint32_t)rows * (uint32_t)row_stride);
 #pragma unroll
-      for (int x = 0; x < CPT; ++x) {
-        const int ch = tid + THREADS * x;
-        c[x] = *(const uint4 *)(tile_base + (ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8);
-      }
-    } else {
-#pragma unroll
-      for (int x = 0; x < CPT; ++x) {
-        const int ch = tid + THREADS * x;
-        const int r = ch / (D / 8);
-        c[x] = r < valid ? *(const uint4 *)(tile_base + r * row_stride + (ch % (D / 8)) * 8)
-                         : make_uint4(0, 0, 0, 0);
-      }
+    for (int x = 0; x < CPT; ++x) {
+      const int ch = tid + THREADS * x;
+      c[x] = buf_load16(rs, 2u * (uint32_t)((ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8));
     }
   }
   __device__ __forceinline__ void store(u16 *lds, int tid) const {
@@ -1007,7 +1034,7 @@ __device__ __forceinline__ f32x16 dq0_block(const u16 *dsb, const u16 *kst, int 
 #pragma unroll
   for (int kk = 0; kk < TILE / 16; ++kk)
     dq = mfma32(read_tr(dsb, DS_STRIDE, 16 * kk + 4 * g, 32 * wi, lane),
-                sread_tr<D>(kst, 16 * kk + 4 * g, 32 * wj, lane), dq);
+                sread_tr<D, SWZ_CF>(kst, 16 * kk + 4 * g, 32 * wj, lane), dq);
   return dq;
 }
 
@@ -1051,8 +1078,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     const bool with_dq = KV_LDS && dsb != nullptr && kt == 0;
     bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
     if constexpr (KV_LDS) {
-      dma_tile<D>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
-      dma_tile<D>(P.v + koff, k_valid, row_stride, smx.vst, w, lane);
+      dma_tile<D, SWZ_CF>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
+      dma_tile<D, SWZ_CF>(P.v + koff, k_valid, row_stride, smx.vst, w, lane);
     } else {
       load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
       load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
@@ -1165,8 +1192,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       for (int ks = 0; ks < D / 16; ++ks) {
         bf16x8 kop, vop;
         if constexpr (KV_LDS) {
-          kop = sread_rm<D>(smx.kst, j_loc, 16 * ks + 8 * g);
-          vop = sread_rm<D>(smx.vst, j_loc, 16 * ks + 8 * g);
+          kop = sread_rm<D, SWZ_CF>(smx.kst, j_loc, 16 * ks + 8 * g);
+          vop = sread_rm<D, SWZ_CF>(smx.vst, j_loc, 16 * ks + 8 * g);
         } else {
           kop = kreg[ks];
           vop = vreg[ks];
@@ -1181,6 +1208,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       // Query rows past the sequence have dO = 0, hence dA = 0 and dS = 0,
       // and contribute a * 0 to dV: only the diagonal tile needs a mask (the
       // causal one).
+      float carry = 0.0f;       // d_pos: a quad's row-head sums for the next quad
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         float x[8], sg[8], av[8], dsv[8];
@@ -1224,10 +1252,33 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
             if (ib + c_row(8 * hh + e, 0) < j_loc) { av[e] = 0.0f; dsv[e] = 0.0f; }
         }
         if constexpr (POS) {
-          // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0)
+          // element (i, j) -> slot i_loc - j_loc + 63, i_loc = ib + c_row(r, 0).
+          // A register quad holds rows i0 .. i0+3 of the lane's key, so
+          // element (i0 + k) of lane l+k lies on the diagonal of element i0
+          // of lane l: each quad is summed along its diagonals inside the
+          // 16-lane row first (band: lane l adds lanes l+k, k = 0..3, one
+          // atomic per lane).  The six elements of a row's first three lanes
+          // that no band reaches (head: lanes m = 0..2 sum them along the
+          // diagonals of rows i0+3 of lane m) lie on the band diagonals of
+          // lanes 5..7 of the next quad (8 rows further), which adds them;
+          // only the step's last quad flushes its heads itself.  Five LDS
+          // atomics per lane and step instead of sixteen.
           typename A::L *pw = &smx.pwin[phase & 1][g][ib - j_loc + (TILE - 1)];
+          const bool row_head = (lane & 15) < 3;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) atomicAdd(pw + c_row(8 * hh + e, 0), A::lds(dsv[e]));
+          for (int q = 0; q < 2; ++q) {
+            const float *v = dsv + 4 * q;
+            const float band =
+                (((v[0] + row_shl<1>(v[1])) + row_shl<2>(v[2])) + row_shl<3>(v[3])) + carry;
+            const float head = (v[3] + row_shr<1>(v[2])) + row_shr<2>(v[1]);
+            const int at = 16 * hh + 8 * q;             // c_row(8 hh + 4 q, 0)
+            atomicAdd(pw + at, A::lds(band));
+            if (hh == 1 && q == 1) {
+              if (row_head) atomicAdd(pw + at + 3, A::lds(head));
+            } else {
+              carry = row_shr<5>(row_head ? head : 0.0f);
+            }
+          }
         }
         if (TIME) {
           // slow tiles accumulate by bucket straight into the work-group

@@ -86,6 +86,44 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Raw buffer loads: a resource over `bytes` bytes from `base` and a per-lane
+// byte offset; loads at or past `bytes` return 0.  The offset is a plain
+// 32-bit register, so a loop that moves the base keeps one register per load
+// instead of a 64-bit address.  `base` and `bytes` must be the same in every
+// lane of the wave: they are read from the first active lane, which puts the
+// resource in scalar registers (the compiler cannot always prove a work-group
+// item's base uniform and would otherwise loop over lanes around each load).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void *ub = (void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, (int)__builtin_amdgcn_readfirstlane(bytes),
+                                           0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  typedef unsigned u32x4b __attribute__((ext_vector_type(4)));
+  const u32x4b v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// Cross-lane moves inside rows of 16 lanes (DPP on the vector ALU): lane l
+// receives x from lane l + K (row_shl) or l - K (row_shr) of its own row,
+// and 0 where that lane lies outside the row.  Every lane of the row must
+// be active.
+template <int K>
+__device__ __forceinline__ float row_shl(float x) {
+  static_assert(K >= 1 && K <= 15, "row shift");
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+      0, __builtin_bit_cast(int, x), 0x100 + K, 0xF, 0xF, false));
+}
+template <int K>
+__device__ __forceinline__ float row_shr(float x) {
+  static_assert(K >= 1 && K <= 15, "row shift");
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+      0, __builtin_bit_cast(int, x), 0x110 + K, 0xF, 0xF, false));
+}
+
 // sigma(x) = 1 / (1 + e^-x) = 1 / (1 + 2^(-x log2 e)) in fp32 on the
 // hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32).  Saturates cleanly:
 // 2^(+large) = inf gives 0, 2^(-large) = 0 gives 1.
