@@ -362,20 +362,24 @@ template <int D> constexpr int FWD_SWZ = D == 64 ? SWZ_ROWS8 : SWZ_CF;
 
 // Issue the loads of a 64 x D tile (rows of `row_stride` elements from
 // `base`) into `lds`; wave w covers 1/4 of it.  Rows at or beyond `valid`
-// (>= 1) repeat row valid-1: finite data that the caller always masks out.
+// read as zeros (finite data that the caller always masks out): the loads go
+// through a buffer resource that ends after row valid-1, so each lane's
+// offsets are the same for every tile of a given row stride and stay in
+// registers across a loop over tiles (no per-tile address arithmetic).
 template <int D, int K>
 __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid, int row_stride,
                                          u16 *lds, int w, int lane) {
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
   constexpr int IPW = TILE * CPR / 64 / 4;         // load instructions per wave
+  const int rows = valid < TILE ? (valid > 0 ? valid : 0) : TILE;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, 2u * (uint32_t)rows * (uint32_t)row_stride);
 #pragma unroll
   for (int x = 0; x < IPW; ++x) {
     const int pos = (w * IPW + x) * 64 + lane;     // chunk position in LDS
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz_key<D, K>(r);
-    const int rr = r < valid ? r : valid - 1;
-    __builtin_amdgcn_global_load_lds((const void *)(base + rr * row_stride + 8 * c),
-                                     (lds_void *)(lds + (w * IPW + x) * 64 * 8), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(lds + (w * IPW + x) * 64 * 8), 16,
+                                             2u * (uint32_t)(r * row_stride + 8 * c), 0, 0, 0);
   }
 }
 
@@ -1078,8 +1082,12 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     const bool with_dq = KV_LDS && dsb != nullptr && kt == 0;
     bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
     if constexpr (KV_LDS) {
-      dma_tile<D, SWZ_CF>(P.k + koff, k_valid, row_stride, smx.kst, w, lane);
-      dma_tile<D, SWZ_CF>(P.v + koff, k_valid, row_stride, smx.vst, w, lane);
+      // (lane made opaque: the loads' offsets are recomputed here rather
+      // than kept in registers across the whole item loop)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      dma_tile<D, SWZ_CF>(P.k + koff, k_valid, row_stride, smx.kst, w, ln);
+      dma_tile<D, SWZ_CF>(P.v + koff, k_valid, row_stride, smx.vst, w, ln);
     } else {
       load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
       load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
