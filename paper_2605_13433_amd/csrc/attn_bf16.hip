@@ -119,17 +119,28 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
 // entry x - s) for the q-stationary kernels, reversed order (copy s, entry
 // 126 - x - s) for the k-stationary one, whose lanes walk the offsets
 // downwards.  Threads with nothing to store write a never-read pad slot.
-// The entry is multiplied by `scale` (log2 e in the forward's base-2 domain).
-__device__ __forceinline__ float pos_fetch(const KParams &P, int h, int qt, int kt, int tid,
-                                           float scale) {
+// The entry is multiplied by `scale` when stored (1/alpha, or the forward's
+// base-2 factor).  The fetch is an unconditional load (index clamped into
+// the table) whose range check and scale wait for the store: a use right
+// after the load would make the wave wait for it there, and with it for
+// every load it has in flight (the next tile's prefetches).
+struct PosEntry {
+  float raw;
+  bool ok;
+};
+
+__device__ __forceinline__ PosEntry pos_fetch(const KParams &P, int h, int qt, int kt,
+                                              int tid) {
   const int span = 2 * P.N - 1;
   const int idx = (kt - qt) * TILE + P.N - TILE + tid;
-  return (tid < 2 * TILE - 1 && idx >= 0 && idx < span)
-             ? scale * P.pos_w[(int64_t)h * span + idx] : 0.0f;
+  const int ic = idx < 0 ? 0 : (idx < span ? idx : span - 1);
+  return PosEntry{P.pos_w[(int64_t)h * span + ic],
+                  tid < 2 * TILE - 1 && idx >= 0 && idx < span};
 }
 
 template <bool REVERSED>
-__device__ __forceinline__ void pos_store(float v, float *pos, int tid) {
+__device__ __forceinline__ void pos_store(PosEntry e, float scale, float *pos, int tid) {
+  const float v = e.ok ? scale * e.raw : 0.0f;
   const int x = REVERSED ? 2 * TILE - 2 - tid : tid;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
@@ -360,6 +371,36 @@ __device__ __forceinline__ int swz(int r, int c) {
 // Key of the forward's K/V tiles.
 template <int D> constexpr int FWD_SWZ = D == 64 ? SWZ_ROWS8 : SWZ_CF;
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor words over `bytes` bytes from `base` (read from the
+// first active lane, so the descriptor sits in scalar registers).
+__device__ __forceinline__ i32x4 rsrc_words(const void *base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4 r;
+  r[0] = (int)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  r[1] = (int)(__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) & 0xffffu);   // stride 0
+  r[2] = (int)__builtin_amdgcn_readfirstlane(bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// One 16-byte-per-lane buffer load into LDS (lane i's bytes land at LDS
+// address lds + 16 i).  Issued from inline assembly on purpose: the compiler
+// cannot tell which LDS bytes such a load writes, so after the builtin form
+// it makes the wave wait for the load before its next LDS read -- also when
+// that read is of the other buffer, which would turn every prefetch of the
+// next tile into a synchronous load.  The callers wait for these loads
+// themselves (wait_vm) before the barrier that publishes the tile.  The
+// leading s_nop covers the wait states a vector-memory instruction needs
+// after a vector instruction wrote the scalar registers it reads.
+__device__ __forceinline__ void buf_load_lds16(const i32x4 &r, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+
 // Issue the loads of a 64 x D tile (rows of `row_stride` elements from
 // `base`) into `lds`; wave w covers 1/4 of it.  Rows at or beyond `valid`
 // read as zeros (finite data that the caller always masks out): the loads go
@@ -372,16 +413,23 @@ __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
   constexpr int IPW = TILE * CPR / 64 / 4;         // load instructions per wave
   const int rows = valid < TILE ? (valid > 0 ? valid : 0) : TILE;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, 2u * (uint32_t)rows * (uint32_t)row_stride);
+  const i32x4 rs = rsrc_words(base, 2u * (uint32_t)rows * (uint32_t)row_stride);
 #pragma unroll
   for (int x = 0; x < IPW; ++x) {
     const int pos = (w * IPW + x) * 64 + lane;     // chunk position in LDS
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz_key<D, K>(r);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(lds + (w * IPW + x) * 64 * 8), 16,
-                                             2u * (uint32_t)(r * row_stride + 8 * c), 0, 0, 0);
+    buf_load_lds16(rs,
+                   (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) u16 *)(
+                       lds + (w * IPW + x) * 64 * 8),
+                   2u * (uint32_t)(r * row_stride + 8 * c));
   }
 }
+
+// Compiler-only barrier for memory operations: keeps the prefetch loads
+// issued above it from being sunk toward their use in the next step (which
+// would expose their latency there); emits no instruction and no wait.
+__device__ __forceinline__ void issue_fence() { asm volatile("" ::: "memory"); }
 
 // Wait for this wave's outstanding global loads, the LDS-filling ones
 // included (they count as vector memory operations, not LDS operations).
@@ -445,7 +493,7 @@ template <int D, bool POS, bool TIME>
 __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it, u16 *kbuf,
                                                u16 *vbuf, int w, int lane, int tid, int i_loc,
                                                int row_stride, int64_t &ts_start,
-                                               int64_t &ts_i, int64_t &ts_k, float &pos_v) {
+                                               int64_t &ts_i, int64_t &ts_k, PosEntry &pos_v) {
   const int64_t hb = (it.start * P.H + it.h) * D;
   dma_tile<D, FWD_SWZ<D>>(P.k + hb, it.len, row_stride, kbuf, w, lane);
   dma_tile<D, FWD_SWZ<D>>(P.v + hb, it.len, row_stride, vbuf, w, lane);
@@ -455,7 +503,7 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
     ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid, P.inv_alpha);
+  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid);
 }
 
 // ---------------------------------------------------------------- forward
@@ -485,7 +533,7 @@ attn_fwd_kernel(KParams P) {
   Item it = load_item(P, cur);
   int item_no = 0;                            // items done by this work-group
   int64_t ts_start = 0, ts_i = 0, ts_k = 0;
-  float pos_v = 0.0f;
+  PosEntry pos_v{0.0f, false};
   bf16x8 qreg[D / 16];
   {
     const int lane = tid0 & 63, g = lane >> 5, l32 = lane & 31;
@@ -539,7 +587,7 @@ attn_fwd_kernel(KParams P) {
     for (int kt = 0; kt <= qt; ++kt, ++phase) {
       const int pb = phase & 1, fs = phase % 3;
       const bool last = kt == qt;
-      if (POS) pos_store<false>(pos_v, sm.pos[pb], tid);
+      if (POS) pos_store<false>(pos_v, P.inv_alpha, sm.pos[pb], tid);
       if (TIME) {
         bool far = q_far;
         if (tid < TILE) {
@@ -558,7 +606,7 @@ attn_fwd_kernel(KParams P) {
       // atomic's latency allows), older than this step's loads, so that no
       // wait for them also waits for the atomic
       if (kt == (qt > 0 ? qt - 1 : 0) && tid == 0)
-        nxt2 = atomicAdd(P.pop, 1) + 2 * (int)gridDim.x;
+        nxt2 = atomicAdd(P.pop, 1);     // + 2 gridDim.x where it is published
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
@@ -566,11 +614,12 @@ attn_fwd_kernel(KParams P) {
         dma_tile<D, FWD_SWZ<D>>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, P.inv_alpha);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       } else if (has_next) {   // ... or the next item's first one
         fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
                                      tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
       }
+      issue_fence();
       const u16 *kt_lds = sm.tile[pb][0];
       const u16 *vt_lds = sm.tile[pb][1];
 
@@ -650,7 +699,7 @@ attn_fwd_kernel(KParams P) {
 
     // the popped index goes out through the epilogue's barriers; sum the
     // two key halves in the last tile's buffer, store O (bf16)
-    if (tid == 0) sm.next[item_no & 1] = nxt2;
+    if (tid == 0) sm.next[item_no & 1] = nxt2 + 2 * (int)gridDim.x;
     const uint4 no_h[TILE_CHUNKS<D>] = {};
     sum_store_tile<D>((float *)sm.tile[(phase - 1) & 1], oacc, wj == 0, wi, g, l32, tid,
                       P.out0 + ((it.start + (int64_t)qt * TILE) * P.H + h) * D,
@@ -791,12 +840,15 @@ template <> struct TabAcc<true> {
 // that step instead of separating items, while a work-group still takes its
 // next item only when it is nearly free (greedy longest-first assignment).
 // The popped index travels through `nxt` (thread 0) and `slot`.
+// The pop's raw return is kept until take_next adds the grid size (the
+// first gridDim.x items are static), so that no arithmetic on it sits next
+// to the atomic.
 __device__ __forceinline__ void pop_next(const KParams &P, int tid, int &nxt) {
-  if (tid == 0) nxt = atomicAdd(P.pop, 1) + (int)gridDim.x;
+  if (tid == 0) nxt = atomicAdd(P.pop, 1);
 }
 
 __device__ __forceinline__ int take_next(int *slot, int tid, int nxt) {
-  if (tid == 0) *slot = nxt;
+  if (tid == 0) *slot = nxt + (int)gridDim.x;
   lds_barrier();
   return *slot;
 }
@@ -849,7 +901,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       ts_i = P.ts[si.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
       if (tid < TILE) ts_k = P.ts[si.start + (tid < si.len ? tid : si.len - 1)];
     }
-    float pos_v = POS ? pos_fetch(P, h, qt, 0, tid, P.inv_alpha) : 0.0f;
+    PosEntry pos_v = POS ? pos_fetch(P, h, qt, 0, tid) : PosEntry{0.0f, false};
 
     float ts_i32 = 0.0f;
     bool q_far = false;
@@ -874,7 +926,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       lds_barrier();
       kr.store(sm.t.a, tid);
       vr.store(sm.t.b, tid);
-      if (POS) pos_store<false>(pos_v, sm.pos, tid);
+      if (POS) pos_store<false>(pos_v, P.inv_alpha, sm.pos, tid);
       if (TIME) {
         bool far = q_far;
         if (tid < TILE) {
@@ -901,8 +953,9 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
         if (TIME && tid < TILE) ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid, P.inv_alpha);
+        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       }
+      issue_fence();
 
       // S^T quadrant with the position bias as the accumulator's initial
       // value, and dA^T
@@ -1107,7 +1160,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       ts_j = P.ts[r0k + (j_loc < k_valid ? j_loc : k_valid - 1)];
       if (tid < TILE) ts_q = P.ts[r0k + (tid < k_valid ? tid : k_valid - 1)];
     }
-    float pos_v = POS ? pos_fetch(P, h, kt, kt, tid, P.inv_alpha) : 0.0f;
+    PosEntry pos_v = POS ? pos_fetch(P, h, kt, kt, tid) : PosEntry{0.0f, false};
 
     float ts_j32 = 0.0f;
     bool k_far = false;
@@ -1135,7 +1188,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       qr.store(sm.t.a, tid);
       dr.store(sm.t.b, tid);
       if constexpr (POS) {
-        pos_store<true>(pos_v, sm.pos, tid);
+        pos_store<true>(pos_v, P.inv_alpha, sm.pos, tid);
         if (pend_p) atomicAdd(pend_p, pend_v);
         pend_p = nullptr;
         if (qt > kt && tid < 2 * TILE - 1) {
@@ -1174,8 +1227,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
         qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
         dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
         if (TIME && tid < TILE) ts_q = P.ts[r0 + (tid < nv ? tid : nv - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid, P.inv_alpha);
+        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid);
       }
+      issue_fence();
 
       // this lane's queries sit at ib + 8 q4 + c, ib = 32 wi + 4 g; offset
       // j - i = j_loc - ib - i_rel walks the slice downwards, i.e. the
