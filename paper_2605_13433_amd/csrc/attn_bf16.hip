@@ -288,7 +288,9 @@ __device__ __forceinline__ void store_rows(const float *red, int tid, u16 *__res
 // LDS, its partner adds its own in place, then store_rows writes the tile.
 // (The partner reads, adds and writes back its own addresses: LDS float
 // atomics are far slower here even without conflicts.)
-template <int D>
+// With SUM false the writer waves' blocks are the whole result (no partner
+// adds).
+template <int D, bool SUM = true>
 __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D / 32],
                                                bool writer, int half, int g, int l32,
                                                int tid, u16 *__restrict__ out,
@@ -303,14 +305,14 @@ __device__ __forceinline__ void sum_store_tile(float *red, const f32x16 (&acc)[D
         red[(32 * half + c_row(r, g)) * D + 32 * db + l32] = acc[db][r];
   }
   lds_barrier();
-  if (!writer) {
+  if (SUM && !writer) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         red[(32 * half + c_row(r, g)) * D + 32 * db + l32] += acc[db][r];
   }
-  lds_barrier();
+  if (SUM) lds_barrier();
   store_rows<D>(red, tid, out, row_stride, valid, scale, silu, hv);
 }
 
@@ -1052,8 +1054,14 @@ struct DkvSmem {
   // At d=64 the item's stationary K and V tiles live here (swizzled, filled
   // by global-to-LDS loads) instead of in registers, which lets the kernel
   // run three waves per SIMD without the time bias (two with it).
+  // At d=128 only the V tile does (the LDS of two work-groups per CU has
+  // no room for both).
   alignas(16) u16 kst[D == 64 ? TILE * D : 8];
-  alignas(16) u16 vst[D == 64 ? TILE * D : 8];
+  alignas(16) u16 vst[TILE * D];
+  // At d=128 each wave accumulates only one of dV, dK (its query half picks
+  // which), and the waves exchange their step's packed A and dS operands
+  // here: [A or dS][key half][query half][16-query half][lane], 16 KB.
+  alignas(16) uint4 xbuf[D == 128 ? 2 * 2 * 2 * 2 : 1][64];
 };
 
 // Slot x (< 127) of the finished window `prev` of tile offset dt = qt - kt:
@@ -1133,18 +1141,17 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     // `dsb` ([key][query], stride DS_STRIDE) and computes dQ = dS K against
     // the stationary K tile at the item's end (both stay untouched until then).
     const bool with_dq = KV_LDS && dsb != nullptr && kt == 0;
-    bf16x8 kreg[KV_LDS ? 1 : D / 16], vreg[KV_LDS ? 1 : D / 16];
-    if constexpr (KV_LDS) {
+    constexpr bool V_LDS = true;              // V stationary in LDS at both d
+    bf16x8 kreg[KV_LDS ? 1 : D / 16];
+    {
       // (lane made opaque: the loads' offsets are recomputed here rather
       // than kept in registers across the whole item loop)
       int ln = lane;
       asm volatile("" : "+v"(ln));
-      dma_tile<D, SWZ_CF>(P.k + koff, k_valid, row_stride, smx.kst, w, ln);
+      if constexpr (KV_LDS) dma_tile<D, SWZ_CF>(P.k + koff, k_valid, row_stride, smx.kst, w, ln);
       dma_tile<D, SWZ_CF>(P.v + koff, k_valid, row_stride, smx.vst, w, ln);
-    } else {
-      load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
-      load_stationary<D>(P.v + koff, j_loc, k_valid, row_stride, g, vreg);
     }
+    if constexpr (!KV_LDS) load_stationary<D>(P.k + koff, j_loc, k_valid, row_stride, g, kreg);
 
     // every load of the item's start is issued before any of them is used
     // (one memory latency); timestamps of rows past the sequence repeat its
@@ -1176,12 +1183,22 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     typename A::L *my_t = TIME ? tacc + h * P.nb : nullptr;
     typename A::G *dp_item = POS ? (typename A::G *)P.dpos_part + si.start * P.H + h : nullptr;
 
-    f32x16 dk[D / 32], dv[D / 32];
+    // At d=128 (SPLIT) a wave's dK and dV accumulators together would take
+    // 128 registers and hold the kernel to one wave per SIMD: there each
+    // wave keeps one of them for its key half -- dV in the waves of query
+    // half 0, dK in those of half 1 -- in `dv`, over both query halves,
+    // whose packed A and dS operands the waves exchange through LDS.
+    constexpr bool SPLIT = D == 128;
+    f32x16 dk[SPLIT ? 1 : D / 32], dv[D / 32];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) { dk[db][r] = 0.0f; dv[db][r] = 0.0f; }
-    if constexpr (KV_LDS) wait_vm();    // the first step's barriers publish the tiles
+      for (int r = 0; r < 16; ++r) dv[db][r] = 0.0f;
+#pragma unroll
+    for (int db = 0; db < (SPLIT ? 1 : D / 32); ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dk[db][r] = 0.0f;
+    if constexpr (V_LDS) wait_vm();     // the first step's barriers publish the tiles
 
     for (int qt = kt; qt < si.ntiles; ++qt, ++phase) {
       lds_barrier();
@@ -1252,14 +1269,9 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        bf16x8 kop, vop;
-        if constexpr (KV_LDS) {
-          kop = sread_rm<D, SWZ_CF>(smx.kst, j_loc, 16 * ks + 8 * g);
-          vop = sread_rm<D, SWZ_CF>(smx.vst, j_loc, 16 * ks + 8 * g);
-        } else {
-          kop = kreg[ks];
-          vop = vreg[ks];
-        }
+        const bf16x8 kop =
+            KV_LDS ? sread_rm<D, SWZ_CF>(smx.kst, j_loc, 16 * ks + 8 * g) : kreg[KV_LDS ? 0 : ks];
+        const bf16x8 vop = sread_rm<D, SWZ_CF>(smx.vst, j_loc, 16 * ks + 8 * g);
         s = mfma32(read_rm(sm.t.a, ST, 32 * wi + l32, 16 * ks + 8 * g), kop, s);
         da = mfma32(read_rm(sm.t.b, ST, 32 * wi + l32, 16 * ks + 8 * g), vop, da);
       }
@@ -1377,11 +1389,32 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
           *(uint2 *)row = make_uint2(pd.x, pd.y);
           *(uint2 *)(row + 8) = make_uint2(pd.z, pd.w);
         }
+        if constexpr (SPLIT) {
+          smx.xbuf[((0 * 2 + wj) * 2 + wi) * 2 + hh][lane] = pa;
+          smx.xbuf[((1 * 2 + wj) * 2 + wi) * 2 + hh][lane] = pd;
+        } else {
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dv[db] = mfma32(a8, read_tr(sm.t.b, ST, krow, 32 * db, lane), dv[db]);
-          dk[db] = mfma32(d8, read_tr(sm.t.a, ST, krow, 32 * db, lane), dk[db]);
+          for (int db = 0; db < D / 32; ++db) {
+            dv[db] = mfma32(a8, read_tr(sm.t.b, ST, krow, 32 * db, lane), dv[db]);
+            dk[db] = mfma32(d8, read_tr(sm.t.a, ST, krow, 32 * db, lane), dk[db]);
+          }
         }
+      }
+      if constexpr (SPLIT) {
+        // this wave's role (wi): dV += A^T dO or dK += dS^T Q over both
+        // query halves, from the operands of the two waves of its key half
+        lds_barrier();
+        const u16 *src = wi ? sm.t.a : sm.t.b;
+#pragma unroll
+        for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const bf16x8 op = as_bf16x8(smx.xbuf[((wi * 2 + wj) * 2 + qh) * 2 + hh][lane]);
+            const int krow = 32 * qh + 16 * hh + 4 * g;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+              dv[db] = mfma32(op, read_tr(src, ST, krow, 32 * db, lane), dv[db]);
+          }
       }
     }
 
@@ -1399,10 +1432,17 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
                            g, l32, tid, P.dq_out + ooff, P.out_stride, k_valid, P.dqk_scale,
                            fuse, hq.c);
     }
-    sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + ooff,
-                      P.out_stride, k_valid, P.dqk_scale, fuse, qr.c);
-    sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + ooff,
-                      P.out_stride, k_valid, P.inv_n, fuse, dr.c);
+    if constexpr (SPLIT) {
+      sum_store_tile<D, false>(&sm.red[0][0], dv, wi == 1, wj, g, l32, tid, P.out0 + ooff,
+                               P.out_stride, k_valid, P.dqk_scale, fuse, qr.c);
+      sum_store_tile<D, false>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + ooff,
+                               P.out_stride, k_valid, P.inv_n, fuse, dr.c);
+    } else {
+      sum_store_tile<D>(&sm.red[0][0], dk, wi == 0, wj, g, l32, tid, P.out0 + ooff,
+                        P.out_stride, k_valid, P.dqk_scale, fuse, qr.c);
+      sum_store_tile<D>(&sm.red[0][0], dv, wi == 0, wj, g, l32, tid, P.out1 + ooff,
+                        P.out_stride, k_valid, P.inv_n, fuse, dr.c);
+    }
 }
 
 // Work-group start of the kernels that run dK/dV items: zeroed d_time
@@ -1443,7 +1483,7 @@ __device__ __forceinline__ void dkv_kernel_fini(const KParams &P, typename TabAc
 // entries are dK/dV items (k-stationary) and dQ items (flagged,
 // q-stationary) in one longest-first order.
 template <int D, bool POS, bool TIME, bool DET>
-__global__ void __launch_bounds__(THREADS, D == 64 ? 2 : 1)
+__global__ void __launch_bounds__(THREADS, 2)
 attn_bwd_kernel(KParams P) {
   typedef TabAcc<DET> A;
   __shared__ DkvSmem<D, POS, DET> smx;
@@ -1495,7 +1535,7 @@ attn_bwd_dq_kernel(KParams P) {
 // Backward, dK/dV and the table gradients: persistent work-groups pop k-tile
 // items longest first.
 template <int D, bool POS, bool TIME, bool DET>
-__global__ void __launch_bounds__(THREADS, D == 64 ? (TIME ? 2 : 3) : 1)
+__global__ void __launch_bounds__(THREADS, D == 64 ? (TIME ? 2 : 3) : 2)
 attn_bwd_dkv_kernel(KParams P) {
   typedef TabAcc<DET> A;
   __shared__ DkvSmem<D, POS, DET> smx;
