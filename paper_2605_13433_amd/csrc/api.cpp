@@ -189,6 +189,7 @@ Layout make_layout(const Problem &p, bool for_bwd, int dev) {
   L.list_q = take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1));
   L.list_k = for_bwd ? take(sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
   L.list_b = for_bwd ? take(2 * sizeof(WorkEntry) * (size_t)std::max<int64_t>(p.max_entries, 1)) : 0;
+  L.list_p = !for_bwd && fwd_pairs(p) ? take(sizeof(WorkEntry) * (size_t)pair_entries(p)) : 0;
   L.dO = for_bwd ? take(elem * (size_t)p.T * p.H * p.d) : 0;
   const bool bf16_bwd = for_bwd && p.dtype == HSTU_BF16;
   L.num_cu = device_info(dev).num_cu;

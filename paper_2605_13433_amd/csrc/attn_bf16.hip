@@ -129,31 +129,34 @@ struct PosEntry {
   bool ok;
 };
 
+// A slice of `len` entries (2*TILE - 1 for one query tile; the forward's
+// two-tile items take TILE*3 - 1, entry x of the upper tile's slice being
+// entry x + TILE of the lower one's), copies `COPY` floats apart.
 __device__ __forceinline__ PosEntry pos_fetch(const KParams &P, int h, int qt, int kt,
-                                              int tid) {
+                                              int tid, int len = 2 * TILE - 1) {
   const int span = 2 * P.N - 1;
   const int idx = (kt - qt) * TILE + P.N - TILE + tid;
   const int ic = idx < 0 ? 0 : (idx < span ? idx : span - 1);
-  return PosEntry{P.pos_w[(int64_t)h * span + ic],
-                  tid < 2 * TILE - 1 && idx >= 0 && idx < span};
+  return PosEntry{P.pos_w[(int64_t)h * span + ic], tid < len && idx >= 0 && idx < span};
 }
 
-template <bool REVERSED>
+template <bool REVERSED, int COPY = POS_COPY, int LEN = 2 * TILE - 1>
 __device__ __forceinline__ void pos_store(PosEntry e, float scale, float *pos, int tid) {
   const float v = e.ok ? scale * e.raw : 0.0f;
-  const int x = REVERSED ? 2 * TILE - 2 - tid : tid;
+  const int x = REVERSED ? LEN - 1 - tid : tid;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    const bool ok = tid < 2 * TILE - 1 && x >= s;
-    pos[s * POS_COPY + (ok ? x - s : POS_COPY - 1)] = v;
+    const bool ok = tid < LEN && x >= s;
+    pos[s * COPY + (ok ? x - s : COPY - 1)] = v;
   }
 }
 
 // Aligned pointer to 4 consecutive slice entries starting at entry x0 (any
 // x0 >= 0): copy x0 & 3, entry x0 - (x0 & 3).
+template <int COPY = POS_COPY>
 __device__ __forceinline__ const float *pos_lane(const float *pos, int x0) {
   const int s = x0 & 3;
-  return pos + s * POS_COPY + (x0 - s);
+  return pos + s * COPY + (x0 - s);
 }
 
 // Float-exponent index of a time difference held exactly in a float
@@ -194,7 +197,7 @@ __device__ __forceinline__ int time_slot_floats(const KParams &P) { return KTAB 
 // issues the loads of BATCH entries before it stores any, so staging costs a
 // few memory latencies rather than one per entry (a smaller batch where the
 // caller's registers are scarce).
-template <int BATCH>
+template <int BATCH, int NT = THREADS>
 __device__ __forceinline__ void stage_time_heads(const KParams &P, float *dyn, int h0, int nh,
                                                  int tid, float scale) {
   const int per = time_slot_floats(P);
@@ -202,41 +205,42 @@ __device__ __forceinline__ void stage_time_heads(const KParams &P, float *dyn, i
     for (int hl = 0; hl < nh; ++hl) {
       const float *tab = P.time_w + (int64_t)(h0 + hl) * P.nb;
       float *slot = dyn + hl * per;
-      for (int x = tid; x < KTAB; x += THREADS) slot[x] = scale * tab[bucket_of_index(x, P.nb)];
-      for (int x = tid; x < P.nb; x += THREADS) slot[KTAB + x] = scale * tab[x];
+      for (int x = tid; x < KTAB; x += NT) slot[x] = scale * tab[bucket_of_index(x, P.nb)];
+      for (int x = tid; x < P.nb; x += NT) slot[KTAB + x] = scale * tab[x];
     }
     return;
   }
   const int total = nh * per;
-  for (int i0 = tid; i0 < total; i0 += BATCH * THREADS) {
+  for (int i0 = tid; i0 < total; i0 += BATCH * NT) {
     float v[BATCH];
 #pragma unroll
     for (int k = 0; k < BATCH; ++k) {
-      const int i = min(i0 + k * THREADS, total - 1);    // in bounds, used if < total
+      const int i = min(i0 + k * NT, total - 1);         // in bounds, used if < total
       const int hl = i / per, x = i - hl * per;
       const int src = x < KTAB ? bucket_of_index(x, P.nb) : x - KTAB;
       v[k] = P.time_w[(int64_t)(h0 + hl) * P.nb + src];
     }
 #pragma unroll
     for (int k = 0; k < BATCH; ++k) {
-      const int i = i0 + k * THREADS;
+      const int i = i0 + k * NT;
       if (i < total) dyn[i] = scale * v[k];
     }
   }
 }
 
 // Kernel start: every head's tables when they fit (then no per-item staging).
-template <int BATCH>
+template <int BATCH, int NT = THREADS>
 __device__ __forceinline__ void stage_all_heads(const KParams &P, float *dyn, int tid,
                                                 float scale) {
-  if (P.all_heads) stage_time_heads<BATCH>(P, dyn, 0, P.H, tid, scale);
+  if (P.all_heads) stage_time_heads<BATCH, NT>(P, dyn, 0, P.H, tid, scale);
 }
 
 // Item start: the slot of head h (staged now if tables are per item).
+template <int NT = THREADS>
 __device__ __forceinline__ float *item_time_slot(const KParams &P, float *dyn, int h, int tid,
                                                  float scale) {
   if (P.all_heads) return dyn + h * time_slot_floats(P);
-  stage_time_heads<1>(P, dyn, h, 1, tid, scale);
+  stage_time_heads<1, NT>(P, dyn, h, 1, tid, scale);
   return dyn;
 }
 
@@ -404,16 +408,16 @@ __device__ __forceinline__ void buf_load_lds16(const i32x4 &r, uint32_t lds_addr
 }
 
 // Issue the loads of a 64 x D tile (rows of `row_stride` elements from
-// `base`) into `lds`; wave w covers 1/4 of it.  Rows at or beyond `valid`
+// `base`) into `lds`; wave w of NW covers 1/NW of it.  Rows at or beyond `valid`
 // read as zeros (finite data that the caller always masks out): the loads go
 // through a buffer resource that ends after row valid-1, so each lane's
 // offsets are the same for every tile of a given row stride and stay in
 // registers across a loop over tiles (no per-tile address arithmetic).
-template <int D, int K>
+template <int D, int K, int NW = 4>
 __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid, int row_stride,
                                          u16 *lds, int w, int lane) {
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
-  constexpr int IPW = TILE * CPR / 64 / 4;         // load instructions per wave
+  constexpr int IPW = TILE * CPR / 64 / NW;        // load instructions per wave (NW waves)
   const int rows = valid < TILE ? (valid > 0 ? valid : 0) : TILE;
   const i32x4 rs = rsrc_words(base, 2u * (uint32_t)rows * (uint32_t)row_stride);
 #pragma unroll
@@ -461,10 +465,15 @@ __device__ __forceinline__ bf16x8 sread_tr(const u16 *lds, int krow, int ncol, i
 // tile kt+1 streams into the other), per-parity bias slices, a three-slot
 // "far timestamp" flag.  An item's output is summed across waves in the
 // buffer of its last tile.
-template <int D>
+// Position-slice copy stride and slice length of the forward's items of QT
+// query tiles (the stride again 16 mod 64 floats, see POS_COPY).
+template <int QT> constexpr int FWD_POS_COPY = QT == 1 ? POS_COPY : 208;
+template <int QT> constexpr int FWD_POS_LEN = TILE * (QT + 1) - 1;
+
+template <int D, int QT>
 struct FwdSmem {
   u16 tile[2][2][TILE * D];              // [buffer][K, V]
-  alignas(16) float pos[2][4 * POS_COPY];
+  alignas(16) float pos[2][4 * FWD_POS_COPY<QT>];
   alignas(16) float ts32[2][TILE];
   int64_t ts64[2][TILE];
   int flag[3];
@@ -491,24 +500,80 @@ __device__ __forceinline__ Item load_item(const KParams &P, int idx) {
 // Streams an item's first key tile into (kbuf, vbuf) and fetches its bias
 // slice and timestamps into registers.  Timestamps of rows past the
 // sequence repeat its last row (those rows are always masked).
-template <int D, bool POS, bool TIME>
+// Streams an item's first key tile into (kbuf, vbuf) and fetches its bias
+// slice and this lane's timestamps into registers (query tile QT*tile + sub
+// for the lane's wave).  Timestamps of rows past the sequence repeat its last
+// row (those rows are always masked).
+template <int D, bool POS, bool TIME, int QT>
 __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it, u16 *kbuf,
                                                u16 *vbuf, int w, int lane, int tid, int i_loc,
-                                               int row_stride, int64_t &ts_start,
+                                               int sub, int row_stride, int64_t &ts_start,
                                                int64_t &ts_i, int64_t &ts_k, PosEntry &pos_v) {
   const int64_t hb = (it.start * P.H + it.h) * D;
-  dma_tile<D, FWD_SWZ<D>>(P.k + hb, it.len, row_stride, kbuf, w, lane);
-  dma_tile<D, FWD_SWZ<D>>(P.v + hb, it.len, row_stride, vbuf, w, lane);
+  dma_tile<D, FWD_SWZ<D>, 4 * QT>(P.k + hb, it.len, row_stride, kbuf, w, lane);
+  dma_tile<D, FWD_SWZ<D>, 4 * QT>(P.v + hb, it.len, row_stride, vbuf, w, lane);
   if (TIME) {
-    const int q_valid = it.len - it.tile * TILE;
+    const int qt = QT * it.tile + sub;
+    const int q_valid = it.len - qt * TILE;
     ts_start = P.ts[it.start];
-    ts_i = P.ts[it.start + (int64_t)it.tile * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
+    ts_i = P.ts[it.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, it.tile, 0, tid);
+  if (POS) pos_v = pos_fetch(P, it.h, QT * it.tile + QT - 1, 0, tid, FWD_POS_LEN<QT>);
+}
+
+// Cross-wave sum of the O tile of one query tile (waves with `mine` set, in
+// two key halves: `writer` stores, its partner adds) and its coalesced bf16
+// store by all NT threads; rows at or beyond `valid` are not written.
+template <int D, int NT>
+__device__ __forceinline__ void fwd_store_o(float *red, const f32x16 (&acc)[D / 32], bool mine,
+                                            bool writer, int half, int g, int l32, int tid,
+                                            u16 *__restrict__ out, int row_stride, int valid) {
+  lds_barrier();
+  if (mine && writer) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(32 * half + c_row(r, g)) * D + 32 * db + l32] = acc[db][r];
+  }
+  lds_barrier();
+  if (mine && !writer) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(32 * half + c_row(r, g)) * D + 32 * db + l32] += acc[db][r];
+  }
+  lds_barrier();
+  constexpr int CH = TILE * D / 8 / NT;
+#pragma unroll
+  for (int x = 0; x < CH; ++x) {
+    const int ch = tid + NT * x;
+    const int row = ch / (D / 8), c8 = ch % (D / 8);
+    if (row < valid) {
+      const float4 a = *(const float4 *)(red + row * D + 8 * c8);
+      const float4 b = *(const float4 *)(red + row * D + 8 * c8 + 4);
+      uint4 pk;
+      pk.x = pack2(a.x, a.y);
+      pk.y = pack2(a.z, a.w);
+      pk.z = pack2(b.x, b.y);
+      pk.w = pack2(b.z, b.w);
+      *(uint4 *)(out + (int64_t)row * row_stride + 8 * c8) = pk;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- forward
+// An item is QT consecutive query tiles of one head: QT = 1 (four waves, 64
+// rows) or QT = 2 (eight waves, 128 rows) -- with two, every streamed K/V
+// tile serves twice the query rows, which halves the K/V traffic of long
+// sequences (the forward on deep batches is bound by it).  Wave w covers
+// query tile QT*tile + sub (sub = w / 4), query half w & 1 and key half
+// (w / 2) & 1; the item runs over the key tiles of its highest query tile,
+// and a wave whose tile ends earlier (or is past the sequence) idles through
+// the remaining steps' barriers.
+//
 // One work-group barrier per key tile: the barrier of tile kt publishes its
 // DMA-filled buffers and bias slices, and proves every wave is done with
 // tile kt-1, whose buffer then takes tile kt+1.  Items are pipelined: each
@@ -517,12 +582,14 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
 // issued one step before an item's last, and an
 // item's last tile streams the next item's first key tile, query rows, bias
 // slice and timestamps, so no item starts with an exposed memory latency.
-template <int D, bool POS, bool TIME>
-__global__ void __launch_bounds__(THREADS, 2)
+template <int D, bool POS, bool TIME, int QT>
+__global__ void __launch_bounds__(THREADS * QT, QT == 1 ? 2 : 1)
 attn_fwd_kernel(KParams P) {
-  __shared__ FwdSmem<D> sm;
+  constexpr int NT = THREADS * QT, NW = 4 * QT;
+  constexpr int PCOPY = FWD_POS_COPY<QT>, PLEN = FWD_POS_LEN<QT>;
+  __shared__ FwdSmem<D, QT> sm;
   extern __shared__ float dyn[];              // time tables (see item_time_slot)
-  const int n_items = P.ctrl[CTRL_N_ENTRIES] * P.H;
+  const int n_items = P.ctrl[QT == 1 ? CTRL_N_ENTRIES : CTRL_N_PAIRS] * P.H;
   int cur = blockIdx.x;
   // second static item: the list's next G items paired in reverse, so the
   // work-group with the longest first item gets the shortest second one
@@ -540,14 +607,15 @@ attn_fwd_kernel(KParams P) {
   {
     const int lane = tid0 & 63, g = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid0 >> 6);
-    const int i_loc = 32 * (w & 1) + l32;
-    fwd_item_start<D, POS, TIME>(P, it, sm.tile[0][0], sm.tile[0][1], w, lane, tid0, i_loc,
-                                 P.H * D, ts_start, ts_i, ts_k, pos_v);
-    load_stationary<D>(P.q + ((it.start + (int64_t)it.tile * TILE) * P.H + it.h) * D, i_loc,
-                       it.len - it.tile * TILE, P.H * D, g, qreg);
+    const int i_loc = 32 * (w & 1) + l32, sub = w >> 2;
+    fwd_item_start<D, POS, TIME, QT>(P, it, sm.tile[0][0], sm.tile[0][1], w, lane, tid0, i_loc,
+                                     sub, P.H * D, ts_start, ts_i, ts_k, pos_v);
+    const int qt0 = QT * it.tile + sub;
+    load_stationary<D>(P.q + ((it.start + (int64_t)qt0 * TILE) * P.H + it.h) * D, i_loc,
+                       it.len - qt0 * TILE, P.H * D, g, qreg);
   }
   // the tables after the first item's loads: both latencies overlap
-  if (TIME) stage_all_heads<8>(P, dyn, tid0, L2E);
+  if (TIME) stage_all_heads<8, NT>(P, dyn, tid0, L2E);
 
   for (;;) {
     // Lane-derived values are rebuilt per item from an opaque copy of the
@@ -559,10 +627,13 @@ attn_fwd_kernel(KParams P) {
     asm volatile("" : "+s"(row_stride));
     const int lane = tid & 63, g = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wi = w & 1, wj = w >> 1;        // query half, key half
-    const int qt = it.tile, h = it.h;
+    const int wi = w & 1, wj = (w >> 1) & 1, sub = w >> 2;   // query half, key half, tile
+    const int qt = QT * it.tile + sub, h = it.h;
     const int q_valid = it.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
+    const int qt_hi = QT * it.tile + QT - 1;                  // the slice's reference tile
+    const int kt_end = min(qt_hi, (it.len - 1) / TILE);       // the item's last key tile
+    const int pos_x = TILE - 1 + TILE * (QT - 1 - sub);       // slice entry of offset 0
 
     float ts_i32 = 0.0f;
     bool q_far = false;
@@ -571,7 +642,7 @@ attn_fwd_kernel(KParams P) {
       const int64_t rel = ts_i - ts_start;
       ts_i32 = (float)(int32_t)rel;
       q_far = rel >= NEAR || rel <= -NEAR;
-      ktab = item_time_slot(P, dyn, h, tid, L2E);
+      ktab = item_time_slot<NT>(P, dyn, h, tid, L2E);
     }
     const int64_t ts_i_item = ts_i, ts_start_item = ts_start;
 
@@ -586,10 +657,12 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
 
-    for (int kt = 0; kt <= qt; ++kt, ++phase) {
+    for (int kt = 0; kt <= kt_end; ++kt, ++phase) {
       const int pb = phase & 1, fs = phase % 3;
-      const bool last = kt == qt;
-      if (POS) pos_store<false>(pos_v, P.inv_alpha, sm.pos[pb], tid);
+      const bool last = kt == kt_end;          // the item's last step
+      const bool diag = kt == qt;              // this wave's diagonal tile
+      const bool active = kt <= qt;            // this wave has work in the step
+      if (POS) pos_store<false, PCOPY, PLEN>(pos_v, P.inv_alpha, sm.pos[pb], tid);
       if (TIME) {
         bool far = q_far;
         if (tid < TILE) {
@@ -607,19 +680,22 @@ attn_fwd_kernel(KParams P) {
       // pop the item after next one step before the last (as late as the
       // atomic's latency allows), older than this step's loads, so that no
       // wait for them also waits for the atomic
-      if (kt == (qt > 0 ? qt - 1 : 0) && tid == 0)
+      if (kt == (kt_end > 0 ? kt_end - 1 : 0) && tid == 0)
         nxt2 = atomicAdd(P.pop, 1);     // + 2 gridDim.x where it is published
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
-        dma_tile<D, FWD_SWZ<D>>(P.k + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][0], w, lane);
-        dma_tile<D, FWD_SWZ<D>>(P.v + (r0 * P.H + h) * D, k_valid, row_stride, sm.tile[pb ^ 1][1], w, lane);
+        dma_tile<D, FWD_SWZ<D>, NW>(P.k + (r0 * P.H + h) * D, k_valid, row_stride,
+                                    sm.tile[pb ^ 1][0], w, lane);
+        dma_tile<D, FWD_SWZ<D>, NW>(P.v + (r0 * P.H + h) * D, k_valid, row_stride,
+                                    sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
+        if (POS) pos_v = pos_fetch(P, h, qt_hi, kt + 1, tid, PLEN);
       } else if (has_next) {   // ... or the next item's first one
-        fwd_item_start<D, POS, TIME>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w, lane,
-                                     tid, i_loc, row_stride, ts_start, ts_i, ts_k, pos_v);
+        fwd_item_start<D, POS, TIME, QT>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w,
+                                         lane, tid, i_loc, sub, row_stride, ts_start, ts_i,
+                                         ts_k, pos_v);
       }
       issue_fence();
       const u16 *kt_lds = sm.tile[pb][0];
@@ -630,23 +706,29 @@ attn_fwd_kernel(KParams P) {
       // 32 wj + 4 g + 8 q4 + c
       const int kb = 32 * wj + 4 * g;
       f32x16 s;
+      if (active) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-      if (POS) {
-        const float *pl = pos_lane(sm.pos[pb], kb - i_loc + (TILE - 1));
+        for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+        if (POS) {
+          const float *pl = pos_lane<PCOPY>(sm.pos[pb], kb - i_loc + pos_x);
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 pbv = *(const float4 *)(pl + 8 * q4);
-          s[4 * q4 + 0] = pbv.x; s[4 * q4 + 1] = pbv.y;
-          s[4 * q4 + 2] = pbv.z; s[4 * q4 + 3] = pbv.w;
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const float4 pbv = *(const float4 *)(pl + 8 * q4);
+            s[4 * q4 + 0] = pbv.x; s[4 * q4 + 1] = pbv.y;
+            s[4 * q4 + 2] = pbv.z; s[4 * q4 + 3] = pbv.w;
+          }
         }
-      }
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks)
-        s = mfma32(sread_rm<D, FWD_SWZ<D>>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks], s);
-      if (last && has_next)    // the query rows are free: fetch the next item's
-        load_stationary<D>(P.q + ((nit.start + (int64_t)nit.tile * TILE) * P.H + nit.h) * D,
-                           i_loc, nit.len - nit.tile * TILE, row_stride, g, qreg);
+        for (int ks = 0; ks < D / 16; ++ks)
+          s = mfma32(sread_rm<D, FWD_SWZ<D>>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g), qreg[ks],
+                     s);
+      }
+      if (last && has_next) {  // the query rows are free: fetch the next item's
+        const int nqt = QT * nit.tile + sub;
+        load_stationary<D>(P.q + ((nit.start + (int64_t)nqt * TILE) * P.H + nit.h) * D, i_loc,
+                           nit.len - nqt * TILE, row_stride, g, qreg);
+      }
+      if (!active) continue;
 
       // x' = (s + pos/alpha) alpha log2e + time bias', A = silu(x)/N, then
       // O_wi += A V, one 16-key half at a time (half the temporaries live at
@@ -679,9 +761,9 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) av[e] = silu2_over_n(x[e], nl);
         // the diagonal tile is the only one with keys past the query (and
-        // the only one that can hold rows past the sequence, repeated rows
-        // that the same mask removes)
-        if (last) {
+        // the only one that can hold rows past the sequence, zero rows that
+        // the same mask removes)
+        if (diag) {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             if (kb + c_row(8 * hh + e, 0) > i_loc) av[e] = 0.0f;
@@ -694,18 +776,24 @@ attn_fwd_kernel(KParams P) {
         const bf16x8 pa = as_bf16x8(pk);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(pa, sread_tr<D, FWD_SWZ<D>>(vt_lds, 32 * wj + 16 * hh + 4 * g, 32 * db, lane),
+          oacc[db] = mfma32(pa,
+                            sread_tr<D, FWD_SWZ<D>>(vt_lds, 32 * wj + 16 * hh + 4 * g, 32 * db,
+                                                    lane),
                             oacc[db]);
       }
     }
 
     // the popped index goes out through the epilogue's barriers; sum the
-    // two key halves in the last tile's buffer, store O (bf16)
+    // two key halves of each query tile in the last tile's buffer, store O
+    // (bf16)
     if (tid == 0) sm.next[item_no & 1] = nxt2 + 2 * (int)gridDim.x;
-    const uint4 no_h[TILE_CHUNKS<D>] = {};
-    sum_store_tile<D>((float *)sm.tile[(phase - 1) & 1], oacc, wj == 0, wi, g, l32, tid,
-                      P.out0 + ((it.start + (int64_t)qt * TILE) * P.H + h) * D,
-                      row_stride, q_valid, 1.0f, false, no_h);
+#pragma unroll
+    for (int sq = 0; sq < QT; ++sq) {
+      const int tq = QT * it.tile + sq;
+      fwd_store_o<D, NT>((float *)sm.tile[(phase - 1) & 1], oacc, sub == sq, wj == 0, wi, g,
+                         l32, tid, P.out0 + ((it.start + (int64_t)tq * TILE) * P.H + h) * D,
+                         row_stride, it.len - tq * TILE);
+    }
     if (!has_next) break;
     cur = nxt;
     it = nit;
@@ -1561,9 +1649,9 @@ attn_bwd_dkv_kernel(KParams P) {
 
 // ------------------------------------------------------------- launchers
 template <typename K>
-int persistent_grid(K kernel, size_t dyn, int64_t items, int dev) {
+int persistent_grid(K kernel, size_t dyn, int64_t items, int dev, int block = THREADS) {
   int occ = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, THREADS, dyn) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, block, dyn) != hipSuccess ||
       occ < 1)
     occ = 1;
   const int64_t cap = (int64_t)device_info(dev).num_cu * occ;
@@ -1627,6 +1715,23 @@ KParams make_params(const AttnArgs &a, int32_t *pop, const WorkEntry *list) {
     }                                                                         \
   } while (0)
 
+// As HSTU_DISPATCH, with a fourth template argument QT (forward items of QT
+// query tiles).
+#define HSTU_DISPATCH_Q(KERNEL, D, POS, TIME, QT, ...)                              \
+  do {                                                                              \
+    if (D == 64) {                                                                  \
+      if (POS && TIME) { auto kfn = KERNEL<64, true, true, QT>; __VA_ARGS__; }      \
+      else if (POS) { auto kfn = KERNEL<64, true, false, QT>; __VA_ARGS__; }       \
+      else if (TIME) { auto kfn = KERNEL<64, false, true, QT>; __VA_ARGS__; }      \
+      else { auto kfn = KERNEL<64, false, false, QT>; __VA_ARGS__; }               \
+    } else {                                                                        \
+      if (POS && TIME) { auto kfn = KERNEL<128, true, true, QT>; __VA_ARGS__; }     \
+      else if (POS) { auto kfn = KERNEL<128, true, false, QT>; __VA_ARGS__; }      \
+      else if (TIME) { auto kfn = KERNEL<128, false, true, QT>; __VA_ARGS__; }     \
+      else { auto kfn = KERNEL<128, false, false, QT>; __VA_ARGS__; }              \
+    }                                                                               \
+  } while (0)
+
 // As HSTU_DISPATCH, for the kernels that accumulate the table gradients
 // (a fourth template argument: the deterministic fixed-point mode).
 #define HSTU_DISPATCH_TAB(KERNEL, D, POS, TIME, DET, ...)                             \
@@ -1667,10 +1772,19 @@ int current_dev() {
 
 }  // namespace
 
+bool fwd_pairs(const Problem &p) {
+  return p.dtype == HSTU_BF16 && p.d == 64 && p.T >= FWD_PAIR_MIN_AVG_LEN * (int64_t)p.B;
+}
+
 int attn_fwd_grid(const Problem &p, int dev) {
   int grid = 1;
-  HSTU_DISPATCH(attn_fwd_kernel, p.d, p.has_pos, p.has_time,
-                grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
+  if (fwd_pairs(p))
+    HSTU_DISPATCH_Q(attn_fwd_kernel, p.d, p.has_pos, p.has_time, 2,
+                    grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev,
+                                           2 * THREADS));
+  else
+    HSTU_DISPATCH_Q(attn_fwd_kernel, p.d, p.has_pos, p.has_time, 1,
+                    grid = persistent_grid(kfn, q_dyn_bytes(p), p.max_entries * p.H, dev));
   return grid;
 }
 
@@ -1697,13 +1811,18 @@ int attn_bwd_dkv_grid(const Problem &p, int dev) {
 
 hipError_t launch_attn_fwd_bf16(const AttnArgs &a, void *o, hipStream_t s) {
   const char *ws = (const char *)a.ws;
-  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_FWD,
-                          (const WorkEntry *)(ws + a.L.list_q));
-  P.out0 = (u16 *)o;
   const Problem &p = a.p;
+  const bool pairs = fwd_pairs(p);
+  KParams P = make_params(a, (int32_t *)(ws + a.L.ctrl) + CTRL_POP_FWD,
+                          (const WorkEntry *)(ws + (pairs ? a.L.list_p : a.L.list_q)));
+  P.out0 = (u16 *)o;
   const int grid = attn_fwd_grid(p, current_dev());
-  HSTU_DISPATCH(attn_fwd_kernel, p.d, p.has_pos, p.has_time,
-                hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), q_dyn_bytes(p), s, P));
+  if (pairs)
+    HSTU_DISPATCH_Q(attn_fwd_kernel, p.d, p.has_pos, p.has_time, 2,
+                    hipLaunchKernelGGL(kfn, dim3(grid), dim3(2 * THREADS), q_dyn_bytes(p), s, P));
+  else
+    HSTU_DISPATCH_Q(attn_fwd_kernel, p.d, p.has_pos, p.has_time, 1,
+                    hipLaunchKernelGGL(kfn, dim3(grid), dim3(THREADS), q_dyn_bytes(p), s, P));
   return hipGetLastError();
 }
 

@@ -24,6 +24,12 @@ constexpr int DTIME_BINS = 16;
 // (resolution 2^-32, |x| < 2^31).
 constexpr double FIX_ONE = 4294967296.0;
 
+// The bf16 d=64 forward takes items of two query tiles (sharing every
+// streamed K/V tile) when the batch's mean sequence length is at least this
+// (at d=128 the two-tile items, one eight-wave work-group per CU, measured
+// slower).
+constexpr int64_t FWD_PAIR_MIN_AVG_LEN = 256;
+
 // The backward runs as one combined launch while the work list holds fewer
 // than this many (entry, head) items per persistent work-group.
 constexpr int BWD_COMBINED_ITEMS_PER_WG = 4;
@@ -37,6 +43,7 @@ enum CtrlSlot {
   CTRL_POP_BWD = 4,     // pop counter of the combined bf16 backward kernel
   CTRL_N_BWD = 5,       // entries in the combined backward list
   CTRL_STATUS = 6,      // seq_offsets contract status (HSTU_SEQ_* word)
+  CTRL_N_PAIRS = 7,     // (sequence, query-tile pair) entries in the pair list
   CTRL_WORDS = 64
 };
 
@@ -78,7 +85,7 @@ struct Problem {
 // Workspace carve-up; offsets in bytes from the workspace base, each region
 // 256-byte aligned.  Regions with size 0 are absent.
 struct Layout {
-  size_t ctrl, seqinfo, list_q, list_k, list_b, dO, dpos_part, dtime_part, total;
+  size_t ctrl, seqinfo, list_q, list_k, list_b, list_p, dO, dpos_part, dtime_part, total;
   // persistent grids of the bf16 backward kernels (combined, dQ, dK/dV) and
   // whether the combined one runs (small problems) or the other two
   int bwd_grid_both, bwd_grid_dq, bwd_grid_dkv;
@@ -211,6 +218,11 @@ hipError_t launch_sum_parts(const float *part, void *out, int64_t n, int32_t par
                             hipStream_t s);
 hipError_t launch_zero(void *p, size_t bytes, int dev, hipStream_t s);
 
+// Whether the bf16 forward runs on the pair list (two query tiles per item),
+// and that list's capacity: every pair but one per sequence covers two of
+// the sum_b ceil(L_b / 64) <= max_entries tiles.
+bool fwd_pairs(const Problem &p);
+inline int64_t pair_entries(const Problem &p) { return (p.max_entries + p.B) / 2 + 1; }
 // Persistent-grid sizes (work-groups) of the bf16 attention kernels.
 int attn_fwd_grid(const Problem &p, int dev);
 int attn_bwd_grid(const Problem &p, int dev);

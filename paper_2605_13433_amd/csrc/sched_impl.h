@@ -16,6 +16,10 @@
 //     and the dQ kernels.
 //   * k-list: entries (b, kt), cost ntiles_b - kt q-tiles.  Consumed by the
 //     dK/dV kernels.
+//   * pair list (forward calls on deep batches): entries (b, p) for every
+//     pair of query tiles 2p, 2p+1 (the second past the sequence when
+//     ntiles_b is odd), cost ~ p+1; consumed by the bf16 forward's two-tile
+//     items.
 //   * combined backward list: both kinds, dK/dV entries before dQ entries of
 //     equal cost (dQ entries flagged), consumed by the combined bf16
 //     backward kernel.  With `fuse_dq0` set, no sequence gets a dQ entry for
@@ -57,6 +61,8 @@ struct SchedSmem {
   int32_t fill[SCHED_MAX_BINS];       // sequences ranked in bin n so far
   int32_t cstart[SCHED_MAX_BINS];     // cost-major: first entry of cost bin c
   int32_t sstart[SCHED_MAX_BINS];     // sequence-major: first entry of bin n's sequences
+  int32_t cstart_p[SCHED_MAX_BINS / 2 + 1];   // pair list, cost-major: first entry of bin c
+  int32_t sstart_p[SCHED_MAX_BINS];           // pair list, sequence-major: bin n's first
   int32_t total;
   int32_t seq_major;
   int32_t status;                     // HSTU_SEQ_* bits found by the contract check
@@ -68,8 +74,8 @@ struct SchedArgs {
   int64_t T;
   int32_t *ctrl;
   SeqInfo *info;
-  WorkEntry *list_q, *list_k, *list_b;
-  int32_t nbins, cap;
+  WorkEntry *list_q, *list_k, *list_b, *list_p;
+  int32_t nbins, cap, cap_p;
   int32_t H;
   int32_t grid_hint;                  // nominal persistent work-groups
   int32_t fuse_dq0;                   // no dQ entries for first q-tiles
@@ -138,6 +144,20 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
       work += (int64_t)c * n * (n + 1) / 2;
     }
     sm.seq_major = work * a.H >= (int64_t)SCHED_SEQ_MAJOR_SLACK * nt_max * a.grid_hint;
+    // pair list: a sequence of n tiles has (n+1)/2 pair entries; cost bin c
+    // (pair index c-1) holds one entry per sequence with n >= 2c-1, i.e. the
+    // ranks below rank0[2c-1] + count[2c-1]
+    int32_t run_p = 0, ge_p = 0, cost_p = 0;
+    for (int n = a.nbins - 1; n >= 1; --n) {
+      sm.sstart_p[n] = run_p;
+      run_p += sm.count[n] * ((n + 1) / 2);
+    }
+    for (int c = a.nbins / 2; c >= 1; --c) {
+      ge_p += sm.count[2 * c - 1] + (2 * c < a.nbins ? sm.count[2 * c] : 0);
+      sm.cstart_p[c] = cost_p;
+      cost_p += ge_p;
+    }
+    a.ctrl[CTRL_N_PAIRS] = a.list_p ? (run_p < a.cap_p ? run_p : a.cap_p) : 0;
     // Valid offsets never exceed the list capacity; overlapping (invalid)
     // ones can, and then only the first `cap` slots are kept -- every slot
     // below the total is filled exactly once, so the kept prefix is dense.
@@ -155,6 +175,7 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     if (sm.status != 0) {
       a.ctrl[CTRL_N_ENTRIES] = 0;
       a.ctrl[CTRL_N_BWD] = 0;
+      a.ctrl[CTRL_N_PAIRS] = 0;
     }
   }
   __syncthreads();
@@ -167,6 +188,14 @@ __device__ __forceinline__ void build_schedule(const SchedArgs &a, SchedSmem &sm
     const int r = sm.rank0[nt] + atomicAdd(&sm.fill[nt], 1);   // rank, by tile count
     // sequence-major: this sequence's first entry
     const int base = sm.sstart[nt] + (r - sm.rank0[nt]) * nt;
+    if (a.list_p) {
+      const int np = (nt + 1) / 2;
+      const int base_p = sm.sstart_p[nt] + (r - sm.rank0[nt]) * np;
+      for (int t = 0; t < np; ++t) {
+        const int sp = seq_major ? base_p + (np - 1 - t) : sm.cstart_p[t + 1] + r;
+        if (sp < a.cap_p) a.list_p[sp] = WorkEntry{b, t, si.len, 0, si.start};
+      }
+    }
     for (int t = 0; t < nt; ++t) {
       const WorkEntry we{b, t, si.len, 0, si.start};
       const int cq = t + 1;          // q-tile t visits k-tiles 0..t
@@ -209,8 +238,10 @@ inline SchedArgs sched_args(const int64_t *seq_offsets, const Problem &p, void *
   a.list_q = (WorkEntry *)(base + L.list_q);
   a.list_k = L.list_k ? (WorkEntry *)(base + L.list_k) : nullptr;
   a.list_b = L.list_b ? (WorkEntry *)(base + L.list_b) : nullptr;
+  a.list_p = L.list_p ? (WorkEntry *)(base + L.list_p) : nullptr;
   a.nbins = (int)((p.N + TILE - 1) / TILE) + 2;
   a.cap = (int32_t)p.max_entries;
+  a.cap_p = (int32_t)pair_entries(p);
   a.H = p.H;
   a.grid_hint = 4 * L.num_cu;
   a.fuse_dq0 = L.list_b && L.bwd_combined && p.d == 64 ? 1 : 0;

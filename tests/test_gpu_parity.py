@@ -63,6 +63,45 @@ def test_small_bf16(case):
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
+# Mean length >= 256 tokens: the bf16 d=64 forward takes items of two query
+# tiles (the pair list; the d=128 cases run the same batches through the
+# one-tile items).  Odd and even tile counts (the last pair of an odd count
+# has no upper tile), one-tile and empty sequences, L = max_len.
+PAIRS = [
+    ([256, 320, 64, 65, 1, 767, 0, 639], 2, 64, 768, True, True),
+    ([256, 320, 64, 65, 1, 767, 0, 639], 2, 128, 768, True, True),
+    ([300, 1, 511], 3, 64, 512, True, False),
+    ([190, 700, 129], 1, 128, 700, False, True),
+]
+
+
+@pytest.mark.parametrize("case", range(len(PAIRS)))
+def test_pair_items_bf16(case):
+    lengths, H, d, N, pos, time = PAIRS[case]
+    assert sum(lengths) >= 256 * len(lengths)
+    say(f"pair-item bf16 case {case}: lengths={lengths} H={H} d={d} N={N} pos={pos} time={time}")
+    w = inputs.make_workload(lengths, H=H, d=d, N=N, pos=pos, time=time, seed=300 + case)
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def test_pair_items_cover_every_tile():
+    """The 1024-sequence Zipf batch (sequence-major pair list): every row of
+    o is written (o starts as NaN), complementing the sampled parity below."""
+    from paper_2605_13433_amd import hstu
+    from tests.gpu_util import to_dev
+    w = inputs.workload(5)
+    say(f"  pair coverage, workload 5 {w.name}: T={w.T}")
+    q, k, v, u = (to_dev(x) for x in (w.q, w.k, w.v, w.u))
+    off = to_dev(w.seq_offsets)
+    plan = hstu.Plan(q, off, w.N, to_dev(w.pos_w), to_dev(w.time_w), to_dev(w.timestamps),
+                     w.num_buckets, backward=False)
+    plan.o.fill_(float("nan"))
+    f = plan.forward(q, k, v, u, off)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(f.o).all())
+
+
 @pytest.mark.parametrize("d", [32, 64, 128])
 def test_small_f32(d):
     lengths = [1, 70, 0, 33, 128]
