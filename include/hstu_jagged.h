@@ -162,9 +162,10 @@ int hstu_jagged_attn_fwd(const void *q, const void *k, const void *v,
  * GPU it runs on until the process ends; a problem whose forward workspace
  * (hstu_jagged_attn_workspace_bytes(.., for_bwd = 0, ..)) is larger is
  * rejected with HSTU_EWORKSPACE (with 4 MiB: up to about 170 000 work-list
- * entries of 64 tokens, e.g. 10 M tokens of 1024 sequences).  The call
- * itself allocates nothing, records no profiler events, and never waits
- * for the device.  All calls on one GPU share its array: calls that overlap
+ * entries of 64 tokens, e.g. 10 M tokens of 1024 sequences; about 115 000
+ * when the forward pairs query tiles, d = 64 with total_tokens >= 256 B).
+ * The call itself allocates nothing, records no profiler events, and never
+ * waits for the device.  All calls on one GPU share its array: calls that overlap
  * on one GPU (other streams or threads) race and give unspecified results;
  * serialise them.  The seq_offsets status word of such a call lives in that
  * array and is not exposed. */

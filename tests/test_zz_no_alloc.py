@@ -39,9 +39,12 @@ def _both(w):
 
 def test_noalloc_matches_forward_twice_shrinking():
     big = inputs.make_workload([300, 1, 64, 129, 0, 700], H=4, d=64, N=768, seed=700)
+    # mean length >= 256 at d=64: the forward's two-query-tile items
+    pairs = inputs.make_workload([600, 1, 64, 129, 0, 900, 300], H=4, d=64, N=900, seed=703)
     small = inputs.make_workload([65, 2], H=2, d=128, N=128, seed=701)
-    say("no-alloc forward: large batch, then a smaller one (d=64, then d=128)")
+    say("no-alloc forward: large batch, a pair-item batch, then a smaller one (d=64, then d=128)")
     _both(big)
+    _both(pairs)
     _both(small)
     f32 = inputs.make_workload([40, 3], H=2, d=32, N=64, dtype=torch.float32, seed=702)
     _both(f32)
