@@ -347,7 +347,7 @@ def cpu_baseline(w, target_s=20.0):
     for b in order:
         probe.append(int(b))
         acc += pairs[b]
-        if acc >= 2e5:
+        if acc >= 2e6:
             break
     sub = inputs.subset(w, sorted(probe))
     t0 = time.perf_counter()
