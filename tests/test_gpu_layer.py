@@ -92,6 +92,21 @@ def test_layer_split_k_weight_gradients():
     compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
 
 
+def test_layer_split_backward_d64():
+    """A d=64 layer on enough tiles that the attention backward runs as the
+    dK/dV and dQ launches (not the combined one): the dQ kernel's fused
+    silu' store into dh, checked with every other output against the
+    oracle."""
+    rng = np.random.default_rng(78)
+    lengths = [900] + rng.integers(20, 141, size=600).tolist()
+    w = inputs.make_workload(lengths, H=4, d=64, N=960, seed=321, layer_dim=128)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
+    say(f"layer split backward d=64: B={w.B} T={w.T}")
+    got = run_layer(w)
+    compare_layer(w, got, layer_oracle.layer_bwd_workload(w))
+
+
 def test_layer_workload4_full():
     """The 32-sequence layer workload (lengths to 4096) at full size: every
     token row, both weight gradients and both tables against the oracle."""

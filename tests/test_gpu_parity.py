@@ -85,6 +85,27 @@ def test_pair_items_bf16(case):
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
 
 
+# Enough 64-row tiles that the backward runs as two launches (a dK/dV
+# kernel, then a dQ kernel) rather than the combined one, at d=64 with
+# every bias combination: 600 short sequences (one to three tiles) and two
+# long ones (16 and 11 tiles: long runs of streamed tiles through the dQ
+# kernel's double buffers).
+@pytest.mark.parametrize("pos,time", [(True, True), (True, False), (False, True),
+                                      (False, False)])
+def test_split_backward_d64(pos, time):
+    from paper_2605_13433_amd import hstu
+    rng = np.random.default_rng(77)
+    lengths = [1000, 700] + rng.integers(20, 141, size=600).tolist()
+    w = inputs.make_workload(lengths, H=4, d=64, N=1024, pos=pos, time=time, seed=400)
+    say(f"split backward d=64 pos={pos} time={time}: B={w.B} T={w.T}")
+    # the library takes the combined launch below 4 items per work-group of
+    # its grid (CUs x occupancy, at most 4 work-groups per CU here)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
 def test_pair_items_cover_every_tile():
     """The 1024-sequence Zipf batch (sequence-major pair list): every row of
     o is written (o starts as NaN), complementing the sampled parity below."""
