@@ -883,8 +883,9 @@ struct StreamSmem {
 };
 
 // Per-lane running sum of d_time contributions (dS multiplied by log2e, as
-// the dK/dV items carry it) over one float-exponent time index (the lane's pairs visit non-decreasing indices when timestamps are
-// ordered, so a run ends only when its index changes); a finished run goes
+// the dK/dV items carry it) over one float-exponent time index (the lane's
+// pairs visit non-decreasing indices when timestamps are ordered, so a run
+// ends only when its index changes); a finished run goes, divided by log2e,
 // to its bucket of the work-group's histogram `hist`.  A run is opened by
 // the first index of the item's first tile (start), so adding needs no test
 // for an empty run.
