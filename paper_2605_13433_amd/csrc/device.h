@@ -54,12 +54,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) {
   return __builtin_bit_cast(bf16x8, x);
 }
 
-__device__ __forceinline__ bf16x8 join8(uint2 lo, uint2 hi) {
-  uint4 x;
-  x.x = lo.x; x.y = lo.y; x.z = hi.x; x.w = hi.y;
-  return __builtin_bit_cast(bf16x8, x);
-}
-
 // Relative-time bucket: |x| < 4 -> |x|; otherwise four log-spaced buckets per
 // octave, 4*(e-1) + (two bits below the leading one) with e = floor(log2|x|);
 // clamped to nb-1.  Integer-only, so every device and the host agree.
