@@ -70,6 +70,8 @@ CASES = [
     ("bf16 d64 pos+time", [70, 1, 130, 0, 64, 200], 2, 64, 256, torch.bfloat16),
     ("bf16 d128 pos+time", [150, 33, 1, 260], 2, 128, 320, torch.bfloat16),
     ("fp32 d64 pos+time", [40, 1, 75], 2, 64, 96, torch.float32),
+    # mean length >= 256: the d=64 forward's items of two query tiles
+    ("bf16 d64 pairs", [256, 320, 64, 65, 1, 767, 0, 639], 2, 64, 768, torch.bfloat16),
 ]
 
 
@@ -122,6 +124,39 @@ def test_deterministic_backward_repeats_bitwise(idx):
     for n in ("dq", "dk", "dv", "du"):
         assert torch.equal(a[n], c[n]), n
     compare(w, a, 1.0)
+
+
+def test_deterministic_split_backward_d64():
+    """The deterministic tables on the two-launch backward at d=64 with both
+    biases (600 short sequences and two long ones): bitwise equal across
+    calls, equal gradients to the default mode, oracle parity."""
+    rng = np.random.default_rng(79)
+    lengths = [1000, 700] + rng.integers(20, 141, size=600).tolist()
+    w = inputs.make_workload(lengths, H=4, d=64, N=1024, seed=401)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
+    say(f"  deterministic backward, split d=64 B={w.B} T={w.T}")
+    a = run(w, deterministic=True)
+    b = run(w, deterministic=True)
+    for n in ("d_pos", "d_time"):
+        assert torch.equal(_bits(a[n]), _bits(b[n])), n
+    c = run(w, deterministic=False)
+    for n in ("dq", "dk", "dv", "du"):
+        assert torch.equal(a[n], c[n]), n
+    compare(w, a, 1.0)
+
+
+def test_alpha_split_backward_d64():
+    """A non-unit score scale on the two-launch backward at d=64 with both
+    biases (the dK/dV items carry A and dS scaled, so their stores take
+    scale-dependent factors): oracle parity."""
+    rng = np.random.default_rng(80)
+    lengths = [900] + rng.integers(20, 141, size=600).tolist()
+    w = inputs.make_workload(lengths, H=4, d=64, N=960, seed=402)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
+    say(f"  alpha = 0.7, split d=64 B={w.B} T={w.T}")
+    compare(w, run(w, alpha=0.7), 0.7)
 
 
 def test_deterministic_zipf_subset_and_fp32():
