@@ -72,6 +72,8 @@ PAIRS = [
     ([256, 320, 64, 65, 1, 767, 0, 639], 2, 128, 768, True, True),
     ([300, 1, 511], 3, 64, 512, True, False),
     ([190, 700, 129], 1, 128, 700, False, True),
+    ([190, 700, 129], 2, 64, 700, False, True),
+    ([640, 64, 257, 100], 2, 64, 640, False, False),
 ]
 
 
@@ -100,6 +102,21 @@ def test_split_backward_d64(pos, time):
     say(f"split backward d=64 pos={pos} time={time}: B={w.B} T={w.T}")
     # the library takes the combined launch below 4 items per work-group of
     # its grid (CUs x occupancy, at most 4 work-groups per CU here)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
+    got = run_gpu(w)
+    compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+# The same at d=128 (two launches there too), every bias combination.
+@pytest.mark.parametrize("pos,time", [(True, True), (True, False), (False, True),
+                                      (False, False)])
+def test_split_backward_d128(pos, time):
+    from paper_2605_13433_amd import hstu
+    rng = np.random.default_rng(81)
+    lengths = [800, 300] + rng.integers(20, 141, size=600).tolist()
+    w = inputs.make_workload(lengths, H=4, d=128, N=800, pos=pos, time=time, seed=403)
+    say(f"split backward d=128 pos={pos} time={time}: B={w.B} T={w.T}")
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     assert hstu.max_entries(w.B, w.N, w.T) * w.H >= 4 * 4 * n_cu
     got = run_gpu(w)
