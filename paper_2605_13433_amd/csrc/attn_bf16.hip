@@ -835,6 +835,19 @@ struct TileRegs {
       c[x] = buf_load16(rs, 2u * (uint32_t)((ch / (D / 8)) * row_stride + (ch % (D / 8)) * 8));
     }
   }
+  // The 64-row tile `row0_bytes` bytes into a sequence-wide source `rs`
+  // (one head's rows of a whole sequence, built once per item; rows at or
+  // beyond the sequence's length read as zeros), with no per-tile
+  // descriptor: the tile's offset is added to each lane's offset.
+  __device__ __forceinline__ void load_at(__amdgpu_buffer_rsrc_t rs, uint32_t row0_bytes,
+                                          int row_stride, int tid) {
+#pragma unroll
+    for (int x = 0; x < CPT; ++x) {
+      const int ch = tid + THREADS * x;
+      c[x] = buf_load16(rs, row0_bytes + 2u * (uint32_t)((ch / (D / 8)) * row_stride +
+                                                         (ch % (D / 8)) * 8));
+    }
+  }
   __device__ __forceinline__ void store(u16 *lds, int tid) const {
 #pragma unroll
     for (int x = 0; x < CPT; ++x) {
@@ -987,9 +1000,14 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
     bf16x8 qreg[D / 16], doreg[D / 16];
     load_stationary<D>(P.q + qoff, i_loc, q_valid, row_stride, g, qreg);
     load_stationary<D>(P.dO + qoff, i_loc, q_valid, row_stride, g, doreg);
+    // the sequence's K and V rows of head h, each one source for the item
+    const uint32_t seq_bytes = 2u * (uint32_t)si.len * (uint32_t)row_stride;
+    const __amdgpu_buffer_rsrc_t rs_k = make_rsrc(P.k + (si.start * P.H + h) * D, seq_bytes);
+    const __amdgpu_buffer_rsrc_t rs_v = make_rsrc(P.v + (si.start * P.H + h) * D, seq_bytes);
+    const uint32_t tile_bytes = 2u * (uint32_t)TILE * (uint32_t)row_stride;
     TileRegs<D> kr, vr;
-    kr.load(P.k + (si.start * P.H + h) * D, si.len, row_stride, tid);
-    vr.load(P.v + (si.start * P.H + h) * D, si.len, row_stride, tid);
+    kr.load_at(rs_k, 0u, row_stride, tid);
+    vr.load_at(rs_v, 0u, row_stride, tid);
     int64_t ts_start = 0, ts_i = 0, ts_k = 0;
     if (TIME) {
       ts_start = P.ts[si.start];
@@ -1045,8 +1063,8 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       if (kt < qt) {
         const int k_valid = si.len - (kt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(kt + 1) * TILE;
-        kr.load(P.k + (r0 * P.H + h) * D, k_valid, row_stride, tid);
-        vr.load(P.v + (r0 * P.H + h) * D, k_valid, row_stride, tid);
+        kr.load_at(rs_k, (uint32_t)(kt + 1) * tile_bytes, row_stride, tid);
+        vr.load_at(rs_v, (uint32_t)(kt + 1) * tile_bytes, row_stride, tid);
         if (TIME && tid < TILE) ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
       }
@@ -1249,11 +1267,16 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
     // every load of the item's start is issued before any of them is used
     // (one memory latency); timestamps of rows past the sequence repeat its
     // last row (those rows are always masked)
+    // the sequence's Q and dO rows of head h, each one source for the item
+    const uint32_t seq_bytes = 2u * (uint32_t)si.len * (uint32_t)row_stride;
+    const __amdgpu_buffer_rsrc_t rs_q = make_rsrc(P.q + (si.start * P.H + h) * D, seq_bytes);
+    const __amdgpu_buffer_rsrc_t rs_o = make_rsrc(P.dO + (si.start * P.H + h) * D, seq_bytes);
+    const uint32_t tile_bytes = 2u * (uint32_t)TILE * (uint32_t)row_stride;
     TileRegs<D> qr, dr;
     TileRegs<D> hq;                       // h chunks of the first tile's dQ (fused store)
     const int64_t r0k = si.start + (int64_t)kt * TILE;
-    qr.load(P.q + (r0k * P.H + h) * D, k_valid, row_stride, tid);
-    dr.load(P.dO + (r0k * P.H + h) * D, k_valid, row_stride, tid);
+    qr.load_at(rs_q, (uint32_t)kt * tile_bytes, row_stride, tid);
+    dr.load_at(rs_o, (uint32_t)kt * tile_bytes, row_stride, tid);
     int64_t ts_start = 0, ts_j = 0, ts_q = 0;
     if (TIME) {
       ts_start = P.ts[si.start];
@@ -1334,8 +1357,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       if (qt + 1 < si.ntiles) {
         const int nv = si.len - (qt + 1) * TILE;
         const int64_t r0 = si.start + (int64_t)(qt + 1) * TILE;
-        qr.load(P.q + (r0 * P.H + h) * D, nv, row_stride, tid);
-        dr.load(P.dO + (r0 * P.H + h) * D, nv, row_stride, tid);
+        qr.load_at(rs_q, (uint32_t)(qt + 1) * tile_bytes, row_stride, tid);
+        dr.load_at(rs_o, (uint32_t)(qt + 1) * tile_bytes, row_stride, tid);
         if (TIME && tid < TILE) ts_q = P.ts[r0 + (tid < nv ? tid : nv - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid);
       }
