@@ -56,7 +56,9 @@
  * tables and LayerNorm statistics are float32; contractions run on bf16 MFMA
  * with float32 accumulation, a_ij and dS_ij are rounded to bf16 only as MFMA
  * operands; d in {64, 128}.  HSTU_F32: every tensor is float32 and all
- * arithmetic is float32; d in {32, 64, 128}.
+ * arithmetic is float32, except that the two bias-table gradients are
+ * summed in float64 (or 64-bit fixed point, deterministic mode) before
+ * their float32 store; d in {32, 64, 128}.
  *
  * Return codes: 0 on success, else one of the negative HSTU_E* codes below;
  * hstu_last_error() then describes the failure (thread-local string owned by

@@ -436,6 +436,27 @@ __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid
   }
 }
 
+// As dma_tile, from a sequence-wide source `rs` (one head's rows of a whole
+// sequence, built once per item; rows at or beyond the sequence's length
+// read as zeros): the tile `row0_bytes` bytes in, its offset added to each
+// lane's offset (no per-tile descriptor).
+template <int D, int K, int NW = 4>
+__device__ __forceinline__ void dma_tile_at(const i32x4 &rs, uint32_t row0_bytes, int row_stride,
+                                            u16 *lds, int w, int lane) {
+  constexpr int CPR = D / 8;
+  constexpr int IPW = TILE * CPR / 64 / NW;
+#pragma unroll
+  for (int x = 0; x < IPW; ++x) {
+    const int pos = (w * IPW + x) * 64 + lane;
+    const int r = pos / CPR;
+    const int c = (pos % CPR) ^ swz_key<D, K>(r);
+    buf_load_lds16(rs,
+                   (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) u16 *)(
+                       lds + (w * IPW + x) * 64 * 8),
+                   row0_bytes + 2u * (uint32_t)(r * row_stride + 8 * c));
+  }
+}
+
 // Compiler-only barrier for memory operations: keeps the prefetch loads
 // issued above it from being sunk toward their use in the next step (which
 // would expose their latency there); emits no instruction and no wait.
@@ -649,6 +670,11 @@ attn_fwd_kernel(KParams P) {
       ktab = item_time_slot<NT>(P, dyn, h, tid, L2E);
     }
     const int64_t ts_i_item = ts_i, ts_start_item = ts_start;
+    // the item's K and V rows of head h: one source each for its tiles
+    const uint32_t seq_bytes = 2u * (uint32_t)it.len * (uint32_t)row_stride;
+    const uint32_t tile_bytes = 2u * (uint32_t)TILE * (uint32_t)row_stride;
+    const i32x4 rs_k = rsrc_words(P.k + (it.start * P.H + h) * D, seq_bytes);
+    const i32x4 rs_v = rsrc_words(P.v + (it.start * P.H + h) * D, seq_bytes);
 
     int nxt2 = 0;
     const bool has_next = nxt < n_items;
@@ -689,10 +715,10 @@ attn_fwd_kernel(KParams P) {
       if (!last) {         // stream the next key tile into the other buffer
         const int k_valid = it.len - (kt + 1) * TILE;
         const int64_t r0 = it.start + (int64_t)(kt + 1) * TILE;
-        dma_tile<D, FWD_SWZ<D>, NW>(P.k + (r0 * P.H + h) * D, k_valid, row_stride,
-                                    sm.tile[pb ^ 1][0], w, lane);
-        dma_tile<D, FWD_SWZ<D>, NW>(P.v + (r0 * P.H + h) * D, k_valid, row_stride,
-                                    sm.tile[pb ^ 1][1], w, lane);
+        dma_tile_at<D, FWD_SWZ<D>, NW>(rs_k, (uint32_t)(kt + 1) * tile_bytes, row_stride,
+                                       sm.tile[pb ^ 1][0], w, lane);
+        dma_tile_at<D, FWD_SWZ<D>, NW>(rs_v, (uint32_t)(kt + 1) * tile_bytes, row_stride,
+                                       sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
         if (POS) pos_v = pos_fetch(P, h, qt_hi, kt + 1, tid, PLEN);

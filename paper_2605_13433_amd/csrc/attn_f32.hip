@@ -27,8 +27,11 @@ struct F32Params {
   const SeqInfo *info;
   const WorkEntry *list;
   float *out0, *out1, *out2;
-  float *d_pos, *d_time;
-  unsigned long long *fix_pos, *fix_time;   // deterministic mode: fixed-point sums
+  // table-gradient sums in the workspace: double (default mode; many
+  // thousands of terms land on one entry, more than float keeps to 1e-5 of
+  // the table) or 64-bit fixed point (deterministic mode)
+  double *acc_pos, *acc_time;
+  unsigned long long *fix_pos, *fix_time;
   int32_t H, N, nb;
   float inv_n, alpha;
 };
@@ -148,11 +151,11 @@ f32_dkv_kernel(F32Params P) {
       dk[c] = fmaf(ds, qi[c], dk[c]);
     }
     const int64_t xp = (int64_t)h * (2 * (int64_t)P.N - 1) + (j - i + P.N - 1);
-    if (P.d_pos) atomicAdd(&P.d_pos[xp], ds);
+    if (P.acc_pos) atomicAdd(&P.acc_pos[xp], (double)ds);
     if (P.fix_pos) atomicAdd(&P.fix_pos[xp], to_fix(ds));
-    if (P.d_time || P.fix_time) {
+    if (P.acc_time || P.fix_time) {
       const int64_t xt = (int64_t)h * P.nb + time_bucket(P.ts[ri] - P.ts[rj], P.nb);
-      if (P.d_time) atomicAdd(&P.d_time[xt], ds);
+      if (P.acc_time) atomicAdd(&P.acc_time[xt], (double)ds);
       if (P.fix_time) atomicAdd(&P.fix_time[xt], to_fix(ds));
     }
   }
@@ -167,6 +170,13 @@ __global__ void fill_zero_kernel(float *p, int64_t n) {
   for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
        x += (int64_t)gridDim.x * blockDim.x)
     p[x] = 0.0f;
+}
+
+// Double table sums -> float tables.
+__global__ void double_to_float_kernel(const double *acc, float *out, int64_t n) {
+  for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
+       x += (int64_t)gridDim.x * blockDim.x)
+    out[x] = (float)acc[x];
 }
 
 // Fixed-point table sums -> float tables.
@@ -220,25 +230,22 @@ hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
   const char *ws = (const char *)a.ws;
   const Problem &p = a.p;
   const int64_t n_pos = (int64_t)p.H * (2 * (int64_t)p.N - 1), n_time = (int64_t)p.H * p.nb;
-  // deterministic mode: fixed-point staging tables in the workspace
-  unsigned long long *fix_pos =
-      (p.deterministic && d_pos) ? (unsigned long long *)(ws + a.L.dpos_part) : nullptr;
-  unsigned long long *fix_time =
-      (p.deterministic && d_time) ? (unsigned long long *)(ws + a.L.dtime_part) : nullptr;
-  if (d_pos) {
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, d_pos, n_pos);
-    if (fix_pos)
-      hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, (float *)fix_pos,
-                         2 * n_pos);
-  }
-  if (d_time) {
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, d_time, n_time);
-    if (fix_time)
-      hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, (float *)fix_time,
-                         2 * n_time);
-  }
+  // table-shaped staging sums in the workspace (8 bytes per entry): 64-bit
+  // fixed point in the deterministic mode, double otherwise; converted to
+  // the float tables after the dK/dV kernel (zeros when T = 0)
+  void *st_pos = d_pos ? (void *)(ws + a.L.dpos_part) : nullptr;
+  void *st_time = d_time ? (void *)(ws + a.L.dtime_part) : nullptr;
+  if (st_pos)
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, (float *)st_pos, 2 * n_pos);
+  if (st_time)
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(8), dim3(256), 0, s, (float *)st_time, 2 * n_time);
+  unsigned long long *fix_pos = p.deterministic ? (unsigned long long *)st_pos : nullptr;
+  unsigned long long *fix_time = p.deterministic ? (unsigned long long *)st_time : nullptr;
+  double *acc_pos = p.deterministic ? nullptr : (double *)st_pos;
+  double *acc_time = p.deterministic ? nullptr : (double *)st_time;
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.T == 0) return e;
+  if (e != hipSuccess) return e;
+  if (p.T > 0) {
   const dim3 grid((unsigned)(p.max_entries * p.H));
   F32Params P = make_params(a, (const WorkEntry *)(ws + a.L.list_q));
   P.dO = (const float *)dO;
@@ -249,16 +256,22 @@ hipError_t launch_attn_bwd_f32(const AttnArgs &a, const void *dO, void *dq,
   K.dO = (const float *)dO;
   K.out1 = (float *)dk;
   K.out2 = (float *)dv;
-  K.d_pos = fix_pos ? nullptr : d_pos;
-  K.d_time = fix_time ? nullptr : d_time;
+  K.acc_pos = acc_pos;
+  K.acc_time = acc_time;
   K.fix_pos = fix_pos;
   K.fix_time = fix_time;
   HSTU_F32_DISPATCH(f32_dkv_kernel, p.d, grid, s, K);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   if (fix_pos)
     hipLaunchKernelGGL(fix_to_float_kernel, dim3(64), dim3(256), 0, s, fix_pos, d_pos, n_pos);
   if (fix_time)
     hipLaunchKernelGGL(fix_to_float_kernel, dim3(8), dim3(256), 0, s, fix_time, d_time, n_time);
+  if (acc_pos)
+    hipLaunchKernelGGL(double_to_float_kernel, dim3(64), dim3(256), 0, s, acc_pos, d_pos, n_pos);
+  if (acc_time)
+    hipLaunchKernelGGL(double_to_float_kernel, dim3(8), dim3(256), 0, s, acc_time, d_time,
+                       n_time);
   return hipGetLastError();
 }
 
