@@ -136,12 +136,17 @@ struct PosEntry {
 // A slice of `len` entries (2*TILE - 1 for one query tile; the forward's
 // two-tile items take TILE*3 - 1, entry x of the upper tile's slice being
 // entry x + TILE of the lower one's), copies `COPY` floats apart.
-__device__ __forceinline__ PosEntry pos_fetch(const KParams &P, int h, int qt, int kt,
-                                              int tid, int len = 2 * TILE - 1) {
+// The table of head h as a buffer source (entries outside it read as 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pos_source(const KParams &P, int h) {
   const int span = 2 * P.N - 1;
-  const int idx = (kt - qt) * TILE + P.N - TILE + tid;
-  const int ic = idx < 0 ? 0 : (idx < span ? idx : span - 1);
-  return PosEntry{P.pos_w[(int64_t)h * span + ic], tid < len && idx >= 0 && idx < span};
+  return make_rsrc(P.pos_w + (int64_t)h * span, 4u * (uint32_t)span);
+}
+
+__device__ __forceinline__ PosEntry pos_fetch(__amdgpu_buffer_rsrc_t rs, int N, int qt, int kt,
+                                              int tid, int len = 2 * TILE - 1) {
+  const int idx = (kt - qt) * TILE + N - TILE + tid;    // < 0 or past the table: reads 0
+  const uint32_t raw = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)(4u * (uint32_t)idx), 0, 0);
+  return PosEntry{__uint_as_float(raw), tid < len};
 }
 
 template <bool REVERSED, int COPY = POS_COPY, int LEN = 2 * TILE - 1>
@@ -395,6 +400,11 @@ __device__ __forceinline__ i32x4 rsrc_words(const void *base, uint32_t bytes) {
   return r;
 }
 
+// LDS byte address of a pointer into the work-group's shared memory: the
+// low 32 bits of its generic address (the shared aperture begins at a
+// multiple of 2^32), without the null test an address-space cast emits.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)p; }
+
 // One 16-byte-per-lane buffer load into LDS (lane i's bytes land at LDS
 // address lds + 16 i).  Issued from inline assembly on purpose: the compiler
 // cannot tell which LDS bytes such a load writes, so after the builtin form
@@ -430,8 +440,7 @@ __device__ __forceinline__ void dma_tile(const u16 *__restrict__ base, int valid
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz_key<D, K>(r);
     buf_load_lds16(rs,
-                   (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) u16 *)(
-                       lds + (w * IPW + x) * 64 * 8),
+                   lds_addr(lds + (w * IPW + x) * 64 * 8),
                    2u * (uint32_t)(r * row_stride + 8 * c));
   }
 }
@@ -451,8 +460,7 @@ __device__ __forceinline__ void dma_tile_at(const i32x4 &rs, uint32_t row0_bytes
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz_key<D, K>(r);
     buf_load_lds16(rs,
-                   (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) u16 *)(
-                       lds + (w * IPW + x) * 64 * 8),
+                   lds_addr(lds + (w * IPW + x) * 64 * 8),
                    row0_bytes + 2u * (uint32_t)(r * row_stride + 8 * c));
   }
 }
@@ -544,7 +552,8 @@ __device__ __forceinline__ void fwd_item_start(const KParams &P, const Item &it,
     ts_i = P.ts[it.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
     if (tid < TILE) ts_k = P.ts[it.start + (tid < it.len ? tid : it.len - 1)];
   }
-  if (POS) pos_v = pos_fetch(P, it.h, QT * it.tile + QT - 1, 0, tid, FWD_POS_LEN<QT>);
+  if (POS) pos_v = pos_fetch(pos_source(P, it.h), P.N, QT * it.tile + QT - 1, 0, tid,
+                             FWD_POS_LEN<QT>);
 }
 
 // Cross-wave sum of the O tile of one query tile (waves with `mine` set, in
@@ -675,6 +684,7 @@ attn_fwd_kernel(KParams P) {
     const uint32_t tile_bytes = 2u * (uint32_t)TILE * (uint32_t)row_stride;
     const i32x4 rs_k = rsrc_words(P.k + (it.start * P.H + h) * D, seq_bytes);
     const i32x4 rs_v = rsrc_words(P.v + (it.start * P.H + h) * D, seq_bytes);
+    const __amdgpu_buffer_rsrc_t rs_pos = pos_source(P, POS ? h : 0);
 
     int nxt2 = 0;
     const bool has_next = nxt < n_items;
@@ -721,7 +731,7 @@ attn_fwd_kernel(KParams P) {
                                        sm.tile[pb ^ 1][1], w, lane);
         if (TIME && tid < TILE)
           ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt_hi, kt + 1, tid, PLEN);
+        if (POS) pos_v = pos_fetch(rs_pos, P.N, qt_hi, kt + 1, tid, PLEN);
       } else if (has_next) {   // ... or the next item's first one
         fwd_item_start<D, POS, TIME, QT>(P, nit, sm.tile[pb ^ 1][0], sm.tile[pb ^ 1][1], w,
                                          lane, tid, i_loc, sub, row_stride, ts_start, ts_i,
@@ -1040,7 +1050,8 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
       ts_i = P.ts[si.start + (int64_t)qt * TILE + (i_loc < q_valid ? i_loc : q_valid - 1)];
       if (tid < TILE) ts_k = P.ts[si.start + (tid < si.len ? tid : si.len - 1)];
     }
-    PosEntry pos_v = POS ? pos_fetch(P, h, qt, 0, tid) : PosEntry{0.0f, false};
+    const __amdgpu_buffer_rsrc_t rs_pos = pos_source(P, POS ? h : 0);
+    PosEntry pos_v = POS ? pos_fetch(rs_pos, P.N, qt, 0, tid) : PosEntry{0.0f, false};
 
     float ts_i32 = 0.0f;
     bool q_far = false;
@@ -1092,7 +1103,7 @@ __device__ __forceinline__ void dq_item(const KParams &P, StreamSmem<D> &sm, flo
         kr.load_at(rs_k, (uint32_t)(kt + 1) * tile_bytes, row_stride, tid);
         vr.load_at(rs_v, (uint32_t)(kt + 1) * tile_bytes, row_stride, tid);
         if (TIME && tid < TILE) ts_k = P.ts[r0 + (tid < k_valid ? tid : k_valid - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt, kt + 1, tid);
+        if (POS) pos_v = pos_fetch(rs_pos, P.N, qt, kt + 1, tid);
       }
       issue_fence();
 
@@ -1309,7 +1320,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       ts_j = P.ts[r0k + (j_loc < k_valid ? j_loc : k_valid - 1)];
       if (tid < TILE) ts_q = P.ts[r0k + (tid < k_valid ? tid : k_valid - 1)];
     }
-    PosEntry pos_v = POS ? pos_fetch(P, h, kt, kt, tid) : PosEntry{0.0f, false};
+    const __amdgpu_buffer_rsrc_t rs_pos = pos_source(P, POS ? h : 0);
+    PosEntry pos_v = POS ? pos_fetch(rs_pos, P.N, kt, kt, tid) : PosEntry{0.0f, false};
 
     float ts_j32 = 0.0f;
     bool k_far = false;
@@ -1386,7 +1398,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
         qr.load_at(rs_q, (uint32_t)(qt + 1) * tile_bytes, row_stride, tid);
         dr.load_at(rs_o, (uint32_t)(qt + 1) * tile_bytes, row_stride, tid);
         if (TIME && tid < TILE) ts_q = P.ts[r0 + (tid < nv ? tid : nv - 1)];
-        if (POS) pos_v = pos_fetch(P, h, qt + 1, kt, tid);
+        if (POS) pos_v = pos_fetch(rs_pos, P.N, qt + 1, kt, tid);
       }
       issue_fence();
 
