@@ -124,10 +124,11 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
 // 126 - x - s) for the k-stationary one, whose lanes walk the offsets
 // downwards.  Threads with nothing to store write a never-read pad slot.
 // The entry is multiplied by `scale` when stored (1/alpha, or the forward's
-// base-2 factor).  The fetch is an unconditional load (index clamped into
-// the table) whose range check and scale wait for the store: a use right
-// after the load would make the wave wait for it there, and with it for
-// every load it has in flight (the next tile's prefetches).
+// base-2 factor).  The fetch is an unconditional load through a buffer
+// resource over the head's table (an index outside it reads 0, so no clamp)
+// whose scale waits for the store: a use right after the load would make
+// the wave wait for it there, and with it for every load it has in flight
+// (the next tile's prefetches).
 struct PosEntry {
   float raw;
   bool ok;
