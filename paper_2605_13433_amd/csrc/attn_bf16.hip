@@ -875,7 +875,9 @@ struct TileRegs {
   // The 64-row tile `row0_bytes` bytes into a sequence-wide source `rs`
   // (one head's rows of a whole sequence, built once per item; rows at or
   // beyond the sequence's length read as zeros), with no per-tile
-  // descriptor: the tile's offset is added to each lane's offset.
+  // descriptor: the tile's offset is added to each lane's offset.  Sizes
+  // and offsets fit 32 bits: a sequence's rows span at most 2 * 65536 *
+  // (64 * 128) bytes = 2^30 under the library's limits on max_len, H, d.
   __device__ __forceinline__ void load_at(__amdgpu_buffer_rsrc_t rs, uint32_t row0_bytes,
                                           int row_stride, int tid) {
 #pragma unroll
