@@ -25,6 +25,11 @@ Recipe (fixed, so every run of a given workload sees identical bits):
     (bf16 by round-to-nearest-even, or kept as float32).
   * pos_w [H, 2N-1] and time_w [H, num_buckets] ~ N(0, 0.1) in float32.
   * layer workload: x ~ N(0, 1); w1, w2 ~ N(0, 1/fan_in).
+  * device workload (sizes whose inputs are too large to draw and move from
+    the host): lengths and timestamps as above, then pos_w and time_w on the
+    host; q, k, v, u, dy ~ N(0, 1) in float32 drawn on the GPU, in that
+    order, by torch's Philox generator seeded with `seed`, rounded once to
+    the compute dtype.
 """
 from __future__ import annotations
 
@@ -60,7 +65,8 @@ WORKLOADS = {
 
 @dataclass
 class Workload:
-    """One batch of jagged inputs; tensors live on the CPU."""
+    """One batch of jagged inputs; tensors live on the CPU (q, k, v, u and dy
+    on the GPU for a device workload)."""
     B: int
     H: int
     d: int
@@ -191,8 +197,54 @@ def workload(index: int, seed: Optional[int] = None) -> Workload:
                  spec.get("D_model") if spec.get("layer") else None)
 
 
+def device_workload(lengths, H, d, N, dtype=torch.bfloat16, seed=0,
+                    num_buckets=NUM_TIME_BUCKETS, rab_std=RAB_STD, device="cuda",
+                    name="device") -> Workload:
+    """Inputs for explicit lengths with q, k, v, u and dy drawn on `device`
+    (both biases; seq_offsets, timestamps and tables stay on the host)."""
+    rng = np.random.default_rng(seed)
+    lengths = np.asarray(lengths, dtype=np.int64)
+    offsets = np.zeros(len(lengths) + 1, dtype=np.int64)
+    np.cumsum(lengths, out=offsets[1:])
+    T = int(offsets[-1])
+    ts = timestamps_for(rng, lengths)
+    pos_w = torch.from_numpy(_normal(rng, (H, 2 * N - 1), rab_std))
+    time_w = torch.from_numpy(_normal(rng, (H, num_buckets), rab_std))
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+
+    def draw(shape):
+        x = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+        return x.to(dtype) if dtype != torch.float32 else x
+
+    q, k, v, u = (draw((T, H, d)) for _ in range(4))
+    dy = draw((T, H * d))
+    return Workload(B=len(lengths), H=H, d=d, N=N, dtype=dtype, lengths=lengths,
+                    seq_offsets=torch.from_numpy(offsets), q=q, k=k, v=v, u=u,
+                    dy=dy, pos_w=pos_w, time_w=time_w,
+                    timestamps=torch.from_numpy(ts), num_buckets=num_buckets,
+                    name=name)
+
+
+def prefix(w: Workload, seq: int, n: int) -> Workload:
+    """The first `n` rows of sequence `seq` as a one-sequence batch on the
+    host (same N, tables and absolute timestamps)."""
+    start = int(w.seq_offsets[seq])
+    n = min(int(n), int(w.lengths[seq]))
+    rows = torch.arange(start, start + n, dtype=torch.int64)
+    pick = lambda t: None if t is None else t.index_select(0, rows.to(t.device)).cpu()
+    return Workload(B=1, H=w.H, d=w.d, N=w.N, dtype=w.dtype,
+                    lengths=np.array([n], dtype=np.int64),
+                    seq_offsets=torch.tensor([0, n], dtype=torch.int64),
+                    q=pick(w.q), k=pick(w.k), v=pick(w.v), u=pick(w.u),
+                    dy=pick(w.dy), pos_w=w.pos_w, time_w=w.time_w,
+                    timestamps=pick(w.timestamps), num_buckets=w.num_buckets,
+                    name=w.name + "[prefix]")
+
+
 def subset(w: Workload, seqs) -> Workload:
-    """The sub-batch made of sequences `seqs` (same N, tables and bits)."""
+    """The sub-batch made of sequences `seqs` (same N, tables and bits), on
+    the host whatever device `w`'s tensors live on."""
     seqs = np.asarray(seqs, dtype=np.int64)
     off = w.seq_offsets.numpy()
     rows = np.concatenate([np.arange(off[b], off[b + 1]) for b in seqs]) \
@@ -201,7 +253,7 @@ def subset(w: Workload, seqs) -> Workload:
     lengths = w.lengths[seqs]
     offsets = np.zeros(len(seqs) + 1, dtype=np.int64)
     np.cumsum(lengths, out=offsets[1:])
-    pick = lambda t: None if t is None else t.index_select(0, rows_t)
+    pick = lambda t: None if t is None else t.index_select(0, rows_t.to(t.device)).cpu()
     extra = {}
     if "x" in w.extra:   # layer inputs: token rows follow, weights are shared
         extra = dict(x=pick(w.extra["x"]), w1=w.extra["w1"], w2=w.extra["w2"],

@@ -15,7 +15,7 @@ import pytest
 import torch
 
 from oracle import oracle
-from paper_2605_13433_amd import inputs
+from paper_2605_13433_amd import hstu, inputs
 from tests.gpu_util import TOL, check, rows_of, run_gpu, say
 
 pytestmark = pytest.mark.gpu
@@ -294,6 +294,62 @@ def test_long_sequence_d128():
     w = inputs.make_workload(lengths, H=2, d=128, N=4096, seed=410)
     got = run_gpu(w)
     compare(w, got, oracle.fwd_workload(w), oracle.bwd_workload(w))
+
+
+def test_max_size_batch():
+    """Every size limit at once: four sequences of max_len = 65536 tokens
+    (1024 tiles each) at H = 64 heads of d = 128, so that one head's rows
+    of a sequence span 2^30 bytes (the bound of the kernels' 32-bit
+    in-sequence offsets) and element offsets pass 2^31; H * num_buckets =
+    4096; both biases; then short sequences that start at element 2^31.
+    The inputs are drawn on the GPU.  The oracle cannot run a 65536-token
+    sequence, so it checks what causality isolates exactly: o, y, dQ and dU
+    of the first rows of the first and the last long sequence depend on
+    those rows alone, and the short sequences are checked whole.  Every
+    element of every output must be finite and d_pos zero for j > i."""
+    N, H, d, nb = 65536, 64, 128, 64
+    lengths = [N] * 4 + [333, 1, 64]
+    say(f"max-size batch: lengths={lengths} H={H} d={d} N={N} num_buckets={nb}")
+    w = inputs.device_workload(lengths, H, d, N, seed=430, num_buckets=nb)
+    off = w.seq_offsets.numpy()
+    assert off[4] * H * d == 1 << 31
+    dev = w.q.device
+    offd, ts = w.seq_offsets.to(dev), w.timestamps.to(dev)
+    plan = hstu.Plan(w.q, offd, N, w.pos_w.to(dev), w.time_w.to(dev), ts, nb)
+    f = plan.forward(w.q, w.k, w.v, w.u, offd)
+    g = plan.backward(w.q, w.k, w.v, w.u, offd, w.dy)
+    torch.cuda.synchronize()
+    say("  GPU run done")
+    outs = dict(o=f.o, y=f.y, dq=g.dq, dk=g.dk, dv=g.dv, du=g.du, d_pos=g.d_pos_w,
+                d_time=g.d_time_w)
+    for n, t in outs.items():
+        assert bool(torch.isfinite(t).all()), f"non-finite values in {n}"
+    assert bool((g.d_pos_w[:, N:] == 0).all())
+
+    def rows(t, r):
+        return t.index_select(0, torch.from_numpy(r).to(dev)).to("cpu", torch.float64).numpy()
+
+    tol = TOL[w.dtype]
+    for b, n in ((0, 200), (3, 200)):
+        say(f"  first {n} rows of sequence {b} (rows from {off[b]})")
+        pw = inputs.prefix(w, b, n)
+        ref_f, ref_b = oracle.fwd_workload(pw), oracle.bwd_workload(pw)
+        r = np.arange(off[b], off[b] + n, dtype=np.int64)
+        check("o", rows(f.o, r), ref_f["o"], tol)
+        check("y", rows(f.y, r), ref_f["y"], tol)
+        check("dq", rows(g.dq, r), ref_b["dq"], tol)
+        check("du", rows(g.du, r), ref_b["du"], tol)
+    say("  short sequences 4-6, every output row")
+    sw = inputs.subset(w, [4, 5, 6])
+    ref_f, ref_b = oracle.fwd_workload(sw), oracle.bwd_workload(sw)
+    r = rows_of(w, [4, 5, 6])
+    for n, t in outs.items():
+        if n in ("o", "y"):
+            check(n, rows(t, r), ref_f[n], tol)
+        elif n not in ("d_pos", "d_time"):
+            check(n, rows(t, r), ref_b[n], tol)
+    del plan, f, g, outs, w
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("nb", [32, 1])

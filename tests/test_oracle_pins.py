@@ -287,6 +287,28 @@ def test_causality_bitwise(oracle_lib):
     assert np.array_equal(r["o"][:t], base["o"][:t])
 
 
+def test_prefix_rows_are_exact_on_their_own(oracle_lib):
+    """o, y, dQ and dU of a sequence's first n rows depend on those rows
+    alone (causality; LayerNorm is per row): the oracle on the prefix as a
+    batch of its own, with the same N, gives them bit for bit.  dK and dV of
+    those rows do not (later queries reach them).  This is the premise of
+    the GPU check of the 65536-token batch, and it checks inputs.prefix."""
+    N, H, d = 40, 2, 4
+    w = inputs.make_workload([7, 33, 5], H=H, d=d, N=N, dtype=torch.float64, seed=23)
+    full_f, full_b = oracle_lib.fwd_workload(w), oracle_lib.bwd_workload(w)
+    off = w.seq_offsets.numpy()
+    n = 20
+    p = inputs.prefix(w, 1, n)
+    assert p.lengths.tolist() == [n] and p.N == N
+    pf, pb = oracle_lib.fwd_workload(p), oracle_lib.bwd_workload(p)
+    r = slice(off[1], off[1] + n)
+    for name in ("o", "y"):
+        assert np.array_equal(pf[name], full_f[name][r]), name
+    for name in ("dq", "du"):
+        assert np.array_equal(pb[name], full_b[name][r]), name
+    assert not np.allclose(pb["dk"], full_b["dk"][r])
+
+
 # ------------------------------------------------- P7 isolation / permutation
 def test_isolation_and_permutation(oracle_lib):
     N, H, d = 16, 2, 4
