@@ -352,6 +352,46 @@ def test_max_size_batch():
     torch.cuda.empty_cache()
 
 
+def test_fp32_past_2g_elements():
+    """The fp32 path with element offsets past 2^31: 4096 sequences of 64
+    tokens at H = 64, d = 128 (8.6 GB per operand), then short sequences
+    that start at element 2^31, both biases, inputs drawn on the GPU.  The
+    sequences are independent, so whole sequences at the start, the middle
+    and the end are checked against the oracle; every output element is
+    finite and d_pos zero for j > i."""
+    H, d, N = 64, 128, 333
+    lengths = [64] * 4096 + [333, 1, 64]
+    say(f"fp32 past 2^31 elements: 4096 x 64 + [333, 1, 64] tokens, H={H} d={d} N={N}")
+    w = inputs.device_workload(lengths, H, d, N, dtype=torch.float32, seed=440)
+    off = w.seq_offsets.numpy()
+    assert off[4096] * H * d == 1 << 31
+    dev = w.q.device
+    offd, ts = w.seq_offsets.to(dev), w.timestamps.to(dev)
+    plan = hstu.Plan(w.q, offd, N, w.pos_w.to(dev), w.time_w.to(dev), ts, w.num_buckets)
+    f = plan.forward(w.q, w.k, w.v, w.u, offd)
+    g = plan.backward(w.q, w.k, w.v, w.u, offd, w.dy)
+    torch.cuda.synchronize()
+    say("  GPU run done")
+    outs = dict(o=f.o, y=f.y, dq=g.dq, dk=g.dk, dv=g.dv, du=g.du, d_pos=g.d_pos_w,
+                d_time=g.d_time_w)
+    for n, t in outs.items():
+        assert bool(torch.isfinite(t).all()), f"non-finite values in {n}"
+    assert bool((g.d_pos_w[:, N:] == 0).all())
+    seqs = [0, 2047, 4095, 4096, 4097, 4098]
+    say(f"  sequences {seqs}, every output row")
+    sw = inputs.subset(w, seqs)
+    ref_f, ref_b = oracle.fwd_workload(sw), oracle.bwd_workload(sw)
+    r = torch.from_numpy(rows_of(w, seqs)).to(dev)
+    tol = TOL[w.dtype]
+    for n, t in outs.items():
+        if n in ("d_pos", "d_time"):
+            continue
+        got = t.index_select(0, r).to("cpu", torch.float64).numpy()
+        check(n, got, (ref_f if n in ("o", "y") else ref_b)[n], tol)
+    del plan, f, g, outs, w
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("nb", [32, 1])
 @pytest.mark.parametrize("d,dtype", [(64, torch.bfloat16), (128, torch.bfloat16),
                                      (64, torch.float32)])
