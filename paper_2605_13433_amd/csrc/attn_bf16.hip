@@ -66,7 +66,6 @@ constexpr int POS_COPY = 144;
 constexpr int KTAB = 608;        // float-exponent time index 0..603 (+pad)
 constexpr int32_t NEAR = 1 << 23;  // |ts - ts_start| < NEAR -> float-exponent path
 constexpr float L2E = 1.44269504088896341f;      // log2(e)
-constexpr float INV_L2E = 0.693147180559945309f;  // ln(2) = 1 / log2(e)
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -935,10 +934,11 @@ struct StreamSmem {
 };
 
 // Per-lane running sum of d_time contributions (dS multiplied by log2e, as
-// the dK/dV items carry it) over one float-exponent time index (the lane's
+// the dK/dV items carry it; the table partials keep that factor, which the
+// finalize pass divides out) over one float-exponent time index (the lane's
 // pairs visit non-decreasing indices when timestamps are ordered, so a run
-// ends only when its index changes); a finished run goes, divided by log2e,
-// to its bucket of the work-group's histogram `hist`.  A run is opened by
+// ends only when its index changes); a finished run goes to its bucket of
+// the work-group's histogram `hist`.  A run is opened by
 // the first index of the item's first tile (start), so adding needs no test
 // for an empty run.
 template <typename A>
@@ -949,12 +949,12 @@ struct TimeRun {
   __device__ __forceinline__ void start(int k) { cur = cur < 0 ? k : cur; }
   __device__ __forceinline__ void add(L *hist, int nb, int k, float v) {
     const bool change = k != cur;
-    if (change) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum * INV_L2E));
+    if (change) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum));
     sum = change ? v : sum + v;
     cur = k;
   }
   __device__ __forceinline__ void flush(L *hist, int nb) {
-    if (cur >= 0) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum * INV_L2E));
+    if (cur >= 0) atomicAdd(&hist[bucket_of_index(cur, nb)], A::lds(sum));
     cur = -1;
     sum = 0.0f;
   }
@@ -1451,7 +1451,8 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
       // one 16-query half at a time (half the temporaries live at once).
       // Both are carried multiplied by log2e (A' = u sg with u = x log2e,
       // dS' = dA (sg log2e + A' (1 - sg))): one multiply per element fewer
-      // than natural units; the stores and the table sums divide it out.
+      // than natural units; the stores divide it out, and the table
+      // partials keep it until the finalize pass.
       // Query rows past the sequence have dO = 0, hence dA = 0 and dS = 0,
       // and contribute a * 0 to dV: only the diagonal tile needs a mask (the
       // causal one).
@@ -1521,13 +1522,14 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
 #pragma unroll
           for (int q = 0; q < 2; ++q) {
             const float *v = dsv + 4 * q;
-            const float band =
-                (((v[0] + row_shl<1>(v[1])) + row_shl<2>(v[2])) + row_shl<3>(v[3])) + carry;
+            const float b4 =
+                ((v[0] + row_shl<1>(v[1])) + row_shl<2>(v[2])) + row_shl<3>(v[3]);
+            const float band = hh == 0 && q == 0 ? b4 : b4 + carry;   // first quad: none
             const float head = (v[3] + row_shr<1>(v[2])) + row_shr<2>(v[1]);
             const int at = 16 * hh + 8 * q;             // c_row(8 hh + 4 q, 0)
-            atomicAdd(pw + at, A::lds(band * INV_L2E));
+            atomicAdd(pw + at, A::lds(band));
             if (hh == 1 && q == 1) {
-              if (row_head) atomicAdd(pw + at + 3, A::lds(head * INV_L2E));
+              if (row_head) atomicAdd(pw + at + 3, A::lds(head));
             } else {
               carry = row_shr<5>(row_head ? head : 0.0f);
             }
@@ -1547,7 +1549,7 @@ __device__ __forceinline__ void dkv_item(const KParams &P, DkvSmem<D, POS, DET> 
               // conversion would keep the doubles live across this branch
               float v = dsv[e];
               asm volatile("" : "+v"(v));
-              if (v != 0.0f) atomicAdd(&my_t[tk[e]], A::lds(v * INV_L2E));
+              if (v != 0.0f) atomicAdd(&my_t[tk[e]], A::lds(v));
             }
           }
         }

@@ -103,19 +103,20 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
 
 // Cross-lane moves inside rows of 16 lanes (DPP on the vector ALU): lane l
 // receives x from lane l + K (row_shl) or l - K (row_shr) of its own row,
-// and 0 where that lane lies outside the row.  Every lane of the row must
-// be active.
+// and 0 where that lane lies outside the row (the bound control reads 0
+// there, so no register has to be cleared first).  Every lane of the row
+// must be active.
 template <int K>
 __device__ __forceinline__ float row_shl(float x) {
   static_assert(K >= 1 && K <= 15, "row shift");
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-      0, __builtin_bit_cast(int, x), 0x100 + K, 0xF, 0xF, false));
+      0, __builtin_bit_cast(int, x), 0x100 + K, 0xF, 0xF, true));
 }
 template <int K>
 __device__ __forceinline__ float row_shr(float x) {
   static_assert(K >= 1 && K <= 15, "row shift");
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-      0, __builtin_bit_cast(int, x), 0x110 + K, 0xF, 0xF, false));
+      0, __builtin_bit_cast(int, x), 0x110 + K, 0xF, 0xF, true));
 }
 
 // sigma(x) = 1 / (1 + e^-x) = 1 / (1 + 2^(-x log2 e)) in fp32 on the

@@ -20,9 +20,14 @@ constexpr int TILE = 64;
 constexpr int DTIME_BINS = 16;
 
 // Fixed-point unit of the deterministic backward's table-gradient partials:
-// a partial sum x of N dS is kept as the 64-bit integer round(x * FIX_ONE)
-// (resolution 2^-32, |x| < 2^31).
+// a partial sum x of N log2(e) dS is kept as the 64-bit integer
+// round(x * FIX_ONE) (resolution 2^-32, |x| < 2^31).
 constexpr double FIX_ONE = 4294967296.0;
+
+// The bf16 backward's table-gradient partials hold N log2(e) dS (the dK/dV
+// items carry A and dS in base-2 units); the finalize pass multiplies by
+// TABLE_UNIT / N.
+constexpr double TABLE_UNIT = 0.693147180559945309;   // ln 2 = 1 / log2(e)
 
 // The bf16 d=64 forward takes items of two query tiles (sharing every
 // streamed K/V tile) when the batch's mean sequence length is at least this

@@ -280,8 +280,8 @@ ln_bwd_kernel(const T *__restrict__ dy, const T *__restrict__ u,
 //     work-groups folded theirs into.  Block = 64 consecutive (h, k)
 //     columns; waves stride over the bins.
 // Summation order is fixed, so the result is deterministic given the
-// partials.  `scale` multiplies every entry (1/N: the backward kernel
-// accumulates N dS).
+// partials.  `scale` multiplies every entry (ln 2 / N: the backward kernel
+// accumulates N log2(e) dS).
 // The deterministic backward keeps the partials as 64-bit fixed point
 // (FIX_ONE per unit); they are summed as integers, which no order changes,
 // and converted once.
@@ -440,7 +440,7 @@ hipError_t launch_finalize_tables(const AttnArgs &a, float *d_pos,
                      d_pos ? (const void *)(ws + a.L.dpos_part) : nullptr, p.H, p.N,
                      d_pos, pos_blocks,
                      d_time ? (const void *)(ws + a.L.dtime_part) : nullptr,
-                     DTIME_BINS, width, d_time, 1.0f / (float)p.N);
+                     DTIME_BINS, width, d_time, (float)(TABLE_UNIT / p.N));
   return hipGetLastError();
 }
 
