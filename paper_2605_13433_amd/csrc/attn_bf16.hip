@@ -121,7 +121,8 @@ __device__ __forceinline__ void load_stationary(const u16 *__restrict__ tile_bas
 // entries are one aligned 16-byte load for any lane: forward order (copy s,
 // entry x - s) for the q-stationary kernels, reversed order (copy s, entry
 // 126 - x - s) for the k-stationary one, whose lanes walk the offsets
-// downwards.  Threads with nothing to store write a never-read pad slot.
+// downwards.  Threads past the slice store nothing; the shifted copies of
+// the first entries land in never-read tail slots of the copy before.
 // The entry is multiplied by `scale` when stored (1/alpha, or the forward's
 // base-2 factor).  The fetch is an unconditional load through a buffer
 // resource over the head's table (an index outside it reads 0, so no clamp)
@@ -152,11 +153,14 @@ __device__ __forceinline__ PosEntry pos_fetch(__amdgpu_buffer_rsrc_t rs, int N, 
 template <bool REVERSED, int COPY = POS_COPY, int LEN = 2 * TILE - 1>
 __device__ __forceinline__ void pos_store(PosEntry e, float scale, float *pos, int tid) {
   const float v = e.ok ? scale * e.raw : 0.0f;
-  const int x = REVERSED ? LEN - 1 - tid : tid;
+  if (tid < LEN) {
+    // copy s, entry x - s: one address, the copies at immediate offsets; for
+    // x < s that is one of the last three slots of copy s - 1, which no
+    // read reaches (reads stay below slot LEN <= COPY - 3)
+    static_assert(LEN <= COPY - 3, "copy stride");
+    float *p = pos + (REVERSED ? LEN - 1 - tid : tid);
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const bool ok = tid < LEN && x >= s;
-    pos[s * COPY + (ok ? x - s : COPY - 1)] = v;
+    for (int s = 0; s < 4; ++s) p[s * (COPY - 1)] = v;
   }
 }
 
