@@ -71,11 +71,15 @@ def _code_only(text: str) -> str:
 
 def kernel_source_sha() -> str:
     """Hash of the kernel and launch sources' code (comments and layout
-    ignored): profiles taken from other code are reported as stale."""
+    ignored) and their compiler flags: profiles taken from other code are
+    reported as stale."""
+    from paper_2605_13433_amd import build as _build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2605_13433_amd", "csrc", f), encoding="utf-8") as fh:
             h.update(_code_only(fh.read()).encode())
+        h.update(repr(_build.FILE_FLAGS.get(f, [])).encode())
+    h.update(repr(_build.CFLAGS).encode())
     return h.hexdigest()[:16]
 
 

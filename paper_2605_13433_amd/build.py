@@ -28,6 +28,14 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Wno-unused-variable"]
 
 
+# Per-file flags.  The attention kernels' only uniform-address atomic is a
+# work-group's one-lane pop of its next item; the compiler's atomic
+# optimizer would wrap it in a wave-wide reduction whose broadcast of the
+# returned value waits for the atomic at once (and with it for every load
+# and atomic in flight), instead of where the value is first used, a step
+# later.
+FILE_FLAGS = {"attn_bf16.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+
 # The layer shell's GEMMs run on hipBLASLt.
 LDFLAGS = ["-L/opt/rocm/lib", "-lhipblaslt"]
 
@@ -41,7 +49,8 @@ def _hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *CFLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *CFLAGS, *FILE_FLAGS.get(src, []), "-x", "hip", "-c",
+           os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stderr}")
