@@ -354,6 +354,8 @@ def cpu_baseline(w, target_s=20.0):
         if acc >= 2e6:
             break
     sub = inputs.subset(w, sorted(probe))
+    oracle.fwd_workload(sub)                 # first run: thread pool and pages warm up
+    oracle.bwd_workload(sub)
     t0 = time.perf_counter()
     oracle.fwd_workload(sub)
     oracle.bwd_workload(sub)
