@@ -498,13 +498,11 @@ __device__ __forceinline__ bf16x8 sread_tr(const u16 *lds, int krow, int ncol, i
   return __builtin_bit_cast(bf16x8, x);
 }
 
-// sread_tr at d=64 from a per-lane byte offset (a read's p0 relative to
-// the tile) instead of its coordinates: with the rows-of-8 key the +8-row
-// half sits 8 rows (1 KB) further, so one offset serves both halves.
-__device__ __forceinline__ bf16x8 sread_tr64_at(const u16 *lds, uint32_t off) {
-  const char *p0 = (const char *)lds + off;
-  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p0);
-  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(p0 + 8 * 64 * 2));
+// sread_tr from per-lane byte offsets (the two halves' p0 and p1 relative
+// to the tile) instead of its coordinates.
+__device__ __forceinline__ bf16x8 sread_tr_at(const u16 *lds, uint32_t off0, uint32_t off1) {
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)((const char *)lds + off0));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)((const char *)lds + off1));
   typedef short v8i16 __attribute__((ext_vector_type(8)));
   const v8i16 x = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_bit_cast(bf16x8, x);
@@ -682,18 +680,20 @@ attn_fwd_kernel(KParams P) {
     const int q_valid = it.len - qt * TILE;
     const int i_loc = 32 * wi + l32;
     const int qt_hi = QT * it.tile + QT - 1;                  // the slice's reference tile
-    // d=64: per-lane byte offsets from a tile's base of this wave's K reads
-    // (one per 16-column step) and V transpose reads (one per 32-column
-    // block; its second 16 keys lie 16 rows further, which the rows-of-8
-    // key maps to a fixed 2 KB), kept opaque so that every read is one add
-    // of the buffer's base plus an immediate, not a re-derived address
-    uint32_t koff[D == 64 ? D / 16 : 1], voff[D == 64 ? D / 32 : 1];
-    if constexpr (D == 64) {
+    // Per-lane byte offsets from a tile's base of this wave's K reads (one
+    // per 16-column step) and V transpose reads (per 32-column block, its
+    // rows and rows + 8; the second 16 keys lie 16 rows further, which both
+    // keys map to a fixed distance, as the rows-of-8 key does for rows + 8
+    // at d=64), kept opaque so that every read is one add of the buffer's
+    // base plus an immediate, not a re-derived address
+    constexpr bool V_HI = D == 128;           // rows + 8: an offset of its own
+    uint32_t koff[D / 16], voff[D / 32], vofh[V_HI ? D / 32 : 1];
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        koff[ks] = 2u * (uint32_t)swz<D, FWD_SWZ<D>>(32 * wj + l32, 2 * ks + g);
-        asm volatile("" : "+v"(koff[ks]));
-      }
+    for (int ks = 0; ks < D / 16; ++ks) {
+      koff[ks] = 2u * (uint32_t)swz<D, FWD_SWZ<D>>(32 * wj + l32, 2 * ks + g);
+      asm volatile("" : "+v"(koff[ks]));
+    }
+    {
       const int c = lane & 15;
       const int vrow = 32 * wj + 4 * g + (c >> 2);
 #pragma unroll
@@ -701,6 +701,10 @@ attn_fwd_kernel(KParams P) {
         const int col = 32 * db + ((lane >> 4) & 1) * 16 + 4 * (c & 3);
         voff[db] = 2u * (uint32_t)(swz<D, FWD_SWZ<D>>(vrow, col >> 3) + (col & 7));
         asm volatile("" : "+v"(voff[db]));
+        if constexpr (V_HI) {
+          vofh[db] = 2u * (uint32_t)(swz<D, FWD_SWZ<D>>(vrow + 8, col >> 3) + (col & 7));
+          asm volatile("" : "+v"(vofh[db]));
+        }
       }
     }
     const int kt_end = min(qt_hi, (it.len - 1) / TILE);       // the item's last key tile
@@ -796,11 +800,8 @@ attn_fwd_kernel(KParams P) {
           }
         }
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          const bf16x8 kop = D == 64 ? *(const bf16x8 *)((const char *)kt_lds + koff[D == 64 ? ks : 0])
-                                     : sread_rm<D, FWD_SWZ<D>>(kt_lds, 32 * wj + l32, 16 * ks + 8 * g);
-          s = mfma32(kop, qreg[ks], s);
-        }
+        for (int ks = 0; ks < D / 16; ++ks)
+          s = mfma32(*(const bf16x8 *)((const char *)kt_lds + koff[ks]), qreg[ks], s);
       }
       if (last && has_next) {  // the query rows are free: fetch the next item's
         const int nqt = QT * nit.tile + sub;
@@ -856,9 +857,9 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
           oacc[db] = mfma32(pa,
-                            D == 64 ? sread_tr64_at(vt_lds, voff[D == 64 ? db : 0] + hh * 16 * 64 * 2)
-                                    : sread_tr<D, FWD_SWZ<D>>(vt_lds, 32 * wj + 16 * hh + 4 * g,
-                                                              32 * db, lane),
+                            sread_tr_at(vt_lds, voff[db] + hh * 16 * D * 2,
+                                        (V_HI ? vofh[V_HI ? db : 0] : voff[db] + 8 * D * 2) +
+                                            hh * 16 * D * 2),
                             oacc[db]);
       }
     }
