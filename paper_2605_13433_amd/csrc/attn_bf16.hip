@@ -709,6 +709,15 @@ attn_fwd_kernel(KParams P) {
     }
     const int kt_end = min(qt_hi, (it.len - 1) / TILE);       // the item's last key tile
     const int pos_x = TILE - 1 + TILE * (QT - 1 - sub);       // slice entry of offset 0
+    // this lane's bias-slice reads (4 consecutive entries of one copy, see
+    // pos_lane) at a per-item byte offset from the slice buffer, kept opaque
+    // like the tile offsets
+    uint32_t poff = 0;
+    if (POS) {
+      const int x0 = 32 * wj + 4 * g - i_loc + pos_x;
+      poff = 4u * (uint32_t)((x0 & 3) * PCOPY + (x0 - (x0 & 3)));
+      asm volatile("" : "+v"(poff));
+    }
 
     float ts_i32 = 0.0f;
     bool q_far = false;
@@ -791,7 +800,7 @@ attn_fwd_kernel(KParams P) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[r] = 0.0f;
         if (POS) {
-          const float *pl = pos_lane<PCOPY>(sm.pos[pb], kb - i_loc + pos_x);
+          const float *pl = (const float *)((const char *)sm.pos[pb] + poff);
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
             const float4 pbv = *(const float4 *)(pl + 8 * q4);
