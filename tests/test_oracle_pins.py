@@ -309,6 +309,29 @@ def test_prefix_rows_are_exact_on_their_own(oracle_lib):
     assert not np.allclose(pb["dk"], full_b["dk"][r])
 
 
+def test_device_workload_recipe():
+    """The device-drawn inputs (drawn here on the CPU generator): seeded and
+    reproducible, the documented shapes and dtypes, per-sequence clocks
+    strictly increasing from 0, and inputs.prefix of a whole sequence equal
+    to inputs.subset of it."""
+    kw = dict(H=2, d=8, N=70, seed=3, num_buckets=16, device="cpu")
+    w = inputs.device_workload([5, 0, 70], **kw)
+    w2 = inputs.device_workload([5, 0, 70], **kw)
+    for n in ("q", "k", "v", "u", "dy", "pos_w", "time_w", "timestamps"):
+        assert torch.equal(getattr(w, n), getattr(w2, n)), n
+    assert w.q.shape == (75, 2, 8) and w.dy.shape == (75, 16) and w.q.dtype == torch.bfloat16
+    assert w.pos_w.shape == (2, 139) and w.time_w.shape == (2, 16)
+    ts, off = w.timestamps.numpy(), w.seq_offsets.numpy()
+    for b in range(3):
+        seg = ts[off[b]:off[b + 1]]
+        if len(seg):
+            assert seg[0] == 0 and np.all(np.diff(seg) > 0)
+    p, sb = inputs.prefix(w, 2, 70), inputs.subset(w, [2])
+    assert p.lengths.tolist() == sb.lengths.tolist() == [70]
+    for n in ("q", "k", "v", "u", "dy", "timestamps", "seq_offsets"):
+        assert torch.equal(getattr(p, n), getattr(sb, n)), n
+
+
 # ------------------------------------------------- P7 isolation / permutation
 def test_isolation_and_permutation(oracle_lib):
     N, H, d = 16, 2, 4
